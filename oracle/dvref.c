@@ -1,0 +1,231 @@
+/*
+ * Oracle for the visual-memory path: a plain, slow, obviously correct CPU
+ * implementation in fp64. TEST INFRASTRUCTURE ONLY: it is called by the tests,
+ * by the smoke check and by the benchmark's CPU-baseline leg, never by the
+ * product path. It shares no code, header or table with the GPU library.
+ *
+ * Every function is a literal transcription of a definition of the paper
+ * "Just MLPs: Efficient Visual State Reconstruction for Multimodal Language
+ * Models" (delta-Vision):
+ *   Section 3.1, Eq. 4   adapter A_l(X) = X + phi(X D_l) U_l
+ *   Section 3.1, Eq. 5   embedding adapter  M_l = A_l(E)
+ *   Section 3.1, Eq. 6   recurrent adapter  M_0 = E, M_l = A_l(M_{l-1})
+ *   Section 3.2, Eq. 7   visual K/V = W_{K,l} LN_l(M_l), W_{V,l} LN_l(M_l)
+ *   Section 3.2, Eq. 9   text queries attend to [K^v; K^t], [V^v; V^t] with the
+ *                        causal structure kept for the text part
+ *
+ * Readings where the paper is silent (each is listed with its reason in the
+ * design notes of the repository):
+ *   - weights are stored out x in (the nn.Linear convention): Dw[l] = D_l^T
+ *     [r,d], Uw[l] = U_l^T [d,r], Wk[l], Wv[l] [Hkv*hd, d];
+ *   - LN_l is the backbone's RMSNorm: x * (mean(x^2) + eps)^-1/2 * gamma_l
+ *     (Appendix K names RMSNorm as the frozen norm);
+ *   - phi is SiLU (Section 3.1); the exact erf GELU is accepted as a second
+ *     activation for workloads that name it;
+ *   - the softmax scale is an argument (1/sqrt(hd) by default, as in the
+ *     read-out of Appendix K);
+ *   - query head h reads key/value head h / (Hq/Hkv);
+ *   - no positional rotation is applied to visual keys (Eq. 7 has none).
+ *
+ * Sums run sequentially in fp64. OpenMP only distributes independent output
+ * elements over threads; it changes no arithmetic.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define DVREF_ACT_SILU 0
+#define DVREF_ACT_GELU 1
+
+/* phi of Eq. 4: SiLU(x) = x * sigmoid(x); GELU(x) = x * Phi(x) with the standard normal CDF
+ * Phi(x) = erfc(-x / sqrt 2) / 2 (the erfc form avoids cancellation for negative x). */
+double dvref_act(double x, int act) {
+  if (act == DVREF_ACT_SILU) return x / (1.0 + exp(-x));
+  return 0.5 * x * erfc(-x / sqrt(2.0));
+}
+
+/* Eq. 4 (down half) for every layer: Z[l][t][j] = phi( sum_k X[t][k] * D_l[k][j] )
+ * with D_l[k][j] = Dw[l][j][k].  X [T,d], Dw [L,r,d], Z [L,T,r]. */
+void dvref_down(const double* X, const double* Dw, int64_t T, int d, int L, int r, int act,
+                double* Z) {
+  for (int l = 0; l < L; ++l) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+      for (int j = 0; j < r; ++j) {
+        const double* x = X + t * d;
+        const double* w = Dw + ((int64_t)l * r + j) * d;
+        double s = 0.0;
+        for (int k = 0; k < d; ++k) s += x[k] * w[k];
+        Z[((int64_t)l * T + t) * r + j] = dvref_act(s, act);
+      }
+    }
+  }
+}
+
+/* Eq. 4-5: M_l[t][n] = E[t][n] + sum_j Z_l[t][j] * U_l[j][n], U_l[j][n] = Uw[l][n][j].
+ * E [T,d], Z [L,T,r], Uw [L,d,r], M [L,T,d]. */
+void dvref_memory(const double* E, const double* Z, const double* Uw, int64_t T, int d, int L,
+                  int r, double* M) {
+  for (int l = 0; l < L; ++l) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+      const double* z = Z + ((int64_t)l * T + t) * r;
+      for (int n = 0; n < d; ++n) {
+        const double* u = Uw + ((int64_t)l * d + n) * r;
+        double s = 0.0;
+        for (int j = 0; j < r; ++j) s += z[j] * u[j];
+        M[((int64_t)l * T + t) * d + n] = E[t * d + n] + s;
+      }
+    }
+  }
+}
+
+/* Eq. 6: M_0 = E; layer l (0-based here) applies A_l to the previous memory,
+ * M_l = M_{l-1} + phi(M_{l-1} D_l) U_l, so the first layer's memory is A_0(E).
+ * E [T,d], Dw [L,r,d], Uw [L,d,r], M [L,T,d]. */
+void dvref_memory_recurrent(const double* E, const double* Dw, const double* Uw, int64_t T,
+                            int d, int L, int r, int act, double* M) {
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < T; ++t) {
+    double* z = (double*)malloc(sizeof(double) * (size_t)r);
+    for (int l = 0; l < L; ++l) {
+      const double* prev = (l == 0) ? E + t * d : M + ((int64_t)(l - 1) * T + t) * d;
+      double* cur = M + ((int64_t)l * T + t) * d;
+      for (int j = 0; j < r; ++j) {
+        const double* w = Dw + ((int64_t)l * r + j) * d;
+        double s = 0.0;
+        for (int k = 0; k < d; ++k) s += prev[k] * w[k];
+        z[j] = dvref_act(s, act);
+      }
+      for (int n = 0; n < d; ++n) {
+        const double* u = Uw + ((int64_t)l * d + n) * r;
+        double s = 0.0;
+        for (int j = 0; j < r; ++j) s += z[j] * u[j];
+        cur[n] = prev[n] + s;
+      }
+    }
+    free(z);
+  }
+}
+
+/* RMSNorm read of LN_l: out[n] = x[n] / sqrt( (1/d) sum_k x[k]^2 + eps ) * gamma[n]. */
+void dvref_rmsnorm(const double* x, const double* gamma, int d, double eps, double* out) {
+  double ss = 0.0;
+  for (int k = 0; k < d; ++k) ss += x[k] * x[k];
+  double rho = 1.0 / sqrt(ss / (double)d + eps);
+  for (int n = 0; n < d; ++n) out[n] = x[n] * rho * gamma[n];
+}
+
+/* Eq. 7: Kv_l = LN_l(M_l) W_{K,l}^T and Vv_l = LN_l(M_l) W_{V,l}^T, stored head-major:
+ * Kv[l][b][h][i][c] for token t = b*Nv + i and output channel h*hd + c.
+ * M [L,B*Nv,d], gamma [L,d], Wk, Wv [L,Hkv*hd,d], Kv, Vv [L,B,Hkv,Nv,hd]. */
+void dvref_visual_kv(const double* M, const double* gamma, const double* Wk, const double* Wv,
+                     int B, int Nv, int d, int L, int Hkv, int hd, double eps, double* Kv,
+                     double* Vv) {
+  const int64_t T = (int64_t)B * Nv;
+  const int kv = Hkv * hd;
+  for (int l = 0; l < L; ++l) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+      double* nrm = (double*)malloc(sizeof(double) * (size_t)d);
+      dvref_rmsnorm(M + ((int64_t)l * T + t) * d, gamma + (int64_t)l * d, d, eps, nrm);
+      const int64_t b = t / Nv, i = t % Nv;
+      for (int o = 0; o < kv; ++o) {
+        const double* wk = Wk + ((int64_t)l * kv + o) * d;
+        const double* wv = Wv + ((int64_t)l * kv + o) * d;
+        double sk = 0.0, sv = 0.0;
+        for (int k = 0; k < d; ++k) {
+          sk += nrm[k] * wk[k];
+          sv += nrm[k] * wv[k];
+        }
+        const int h = o / hd, c = o % hd;
+        const int64_t dst = ((((int64_t)l * B + b) * Hkv + h) * Nv + i) * hd + c;
+        Kv[dst] = sk;
+        Vv[dst] = sv;
+      }
+      free(nrm);
+    }
+  }
+}
+
+/* Eq. 9 for one layer. Query (b, i, h) reads key/value head g = h / (Hq/Hkv) and the key set
+ * { visual 0..Nv-1 } U { text 0..q_pos0+i }: every visual key, and text keys up to its own
+ * position (visual tokens precede the text, Eq. 2, so the causal mask never hides them).
+ *   s_j = scale * <Q[b,i,h,:], K_j>,  p = softmax(s),  O[b,i,h,:] = sum_j p_j V_j.
+ * Q, O [B,Nq,Hq,hd]; Kv, Vv [B,Hkv,Nv,hd]; Kt, Vt [B,Hkv,Nkt,hd].
+ * Returns 0, or -1 if a query position has no text key (q_pos0 + Nq > Nkt). */
+int dvref_text_visual_attention(const double* Q, const double* Kv, const double* Vv,
+                                const double* Kt, const double* Vt, double* O, int B, int Hq,
+                                int Hkv, int hd, int Nv, int Nq, int Nkt, int q_pos0,
+                                double scale) {
+  if (q_pos0 < 0 || q_pos0 + Nq > Nkt || Hq % Hkv != 0) return -1;
+  const int G = Hq / Hkv;
+  const int nkeys_max = Nv + Nkt;
+#pragma omp parallel for collapse(3) schedule(static)
+  for (int b = 0; b < B; ++b) {
+    for (int i = 0; i < Nq; ++i) {
+      for (int h = 0; h < Hq; ++h) {
+        const int g = h / G;
+        const double* q = Q + (((int64_t)b * Nq + i) * Hq + h) * hd;
+        const double* kv = Kv + ((int64_t)b * Hkv + g) * (int64_t)Nv * hd;
+        const double* vv = Vv + ((int64_t)b * Hkv + g) * (int64_t)Nv * hd;
+        const double* kt = Kt + ((int64_t)b * Hkv + g) * (int64_t)Nkt * hd;
+        const double* vt = Vt + ((int64_t)b * Hkv + g) * (int64_t)Nkt * hd;
+        const int ntext = q_pos0 + i + 1;
+        const int n = Nv + ntext;
+        double* s = (double*)malloc(sizeof(double) * (size_t)nkeys_max);
+        for (int j = 0; j < n; ++j) {
+          const double* key = (j < Nv) ? kv + (int64_t)j * hd : kt + (int64_t)(j - Nv) * hd;
+          double dot = 0.0;
+          for (int c = 0; c < hd; ++c) dot += q[c] * key[c];
+          s[j] = scale * dot;
+        }
+        double mx = s[0];
+        for (int j = 1; j < n; ++j) mx = s[j] > mx ? s[j] : mx;
+        double denom = 0.0;
+        for (int j = 0; j < n; ++j) {
+          s[j] = exp(s[j] - mx);
+          denom += s[j];
+        }
+        double* o = O + (((int64_t)b * Nq + i) * Hq + h) * hd;
+        for (int c = 0; c < hd; ++c) o[c] = 0.0;
+        for (int j = 0; j < n; ++j) {
+          const double* val = (j < Nv) ? vv + (int64_t)j * hd : vt + (int64_t)(j - Nv) * hd;
+          const double p = s[j] / denom;
+          for (int c = 0; c < hd; ++c) o[c] += p * val[c];
+        }
+        free(s);
+      }
+    }
+  }
+  return 0;
+}
+
+/* Softmax weights of one query row of Eq. 9, exposed so tests can check that they are a
+ * probability distribution. Writes Nv + q_pos0 + i + 1 weights into p. */
+int dvref_attention_weights(const double* Q, const double* Kv, const double* Kt, double* p, int B,
+                            int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt, int q_pos0,
+                            double scale, int b, int i, int h) {
+  if (q_pos0 < 0 || q_pos0 + Nq > Nkt || Hq % Hkv != 0) return -1;
+  const int g = h / (Hq / Hkv);
+  const double* q = Q + (((int64_t)b * Nq + i) * Hq + h) * hd;
+  const double* kv = Kv + ((int64_t)b * Hkv + g) * (int64_t)Nv * hd;
+  const double* kt = Kt + ((int64_t)b * Hkv + g) * (int64_t)Nkt * hd;
+  const int n = Nv + q_pos0 + i + 1;
+  double mx = -INFINITY;
+  for (int j = 0; j < n; ++j) {
+    const double* key = (j < Nv) ? kv + (int64_t)j * hd : kt + (int64_t)(j - Nv) * hd;
+    double dot = 0.0;
+    for (int c = 0; c < hd; ++c) dot += q[c] * key[c];
+    p[j] = scale * dot;
+    mx = p[j] > mx ? p[j] : mx;
+  }
+  double denom = 0.0;
+  for (int j = 0; j < n; ++j) {
+    p[j] = exp(p[j] - mx);
+    denom += p[j];
+  }
+  for (int j = 0; j < n; ++j) p[j] /= denom;
+  return n;
+}

@@ -1,0 +1,114 @@
+"""Seeded synthetic inputs shared by the GPU path, the oracle and the benchmark.
+
+This module draws random numbers and nothing else: it holds none of the
+method's arithmetic. Every tensor is drawn in fp32 from
+``numpy.random.default_rng(SeedSequence([seed, tensor_id, layer]))`` so that any
+single layer of any weight can be regenerated on its own, then rounded to the
+workload dtype (bf16 by round-to-nearest-even). The GPU and the oracle both
+consume exactly these bytes (the oracle widens them to fp64).
+
+Distributions (weights N(0, 1/fan_in), activations N(0, 1)):
+  E      [B*Nv, d]        N(0,1), optional outlier channels multiplied by a scale
+  Dw     [L, r, d]        N(0, 1/d)   down-projection D_l stored out x in
+  Uw     [L, d, r]        N(0, 1/r)   up-projection U_l stored out x in
+  gamma  [L, d]           1 + 0.1 N(0,1)  frozen RMSNorm weight of each layer
+  Wk, Wv [L, Hkv*hd, d]   N(0, 1/d)   frozen key / value projections
+  Q      [L, B, Nq, Hq, hd]    N(0,1)  text queries of each layer
+  Kt, Vt [L, B, Hkv, Nkt, hd]  N(0,1)  text key / value cache of each layer
+  Kv, Vv [L, B, Hkv, Nv, hd]   N(0,1)  cached visual K/V (decode workload only)
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+from typing import Dict, Iterable, Optional, Sequence
+
+import numpy as np
+import torch
+
+from .configs import Workload
+
+TENSOR_IDS = {"E": 1, "Dw": 2, "Uw": 3, "gamma": 4, "Wk": 5, "Wv": 6, "Q": 7, "Kt": 8,
+              "Vt": 9, "Kv": 10, "Vv": 11}
+
+_THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def normal(seed: int, name: str, layer: int, shape: Sequence[int]) -> np.ndarray:
+    """Standard normal fp32 array for (seed, tensor, layer)."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, TENSOR_IDS[name], layer]))
+    return rng.standard_normal(tuple(shape), dtype=np.float32)
+
+
+def torch_dtype(w: Workload) -> torch.dtype:
+    return torch.float32 if w.dtype == "f32" else torch.bfloat16
+
+
+def _to_dtype(a: np.ndarray, dt: torch.dtype) -> torch.Tensor:
+    return torch.from_numpy(a).to(dt)
+
+
+def _per_layer(seed: int, name: str, layers: Sequence[int], shape: Sequence[int], std: float,
+               shift: float, dt: torch.dtype) -> torch.Tensor:
+    def one(l: int) -> torch.Tensor:
+        a = normal(seed, name, l, shape)
+        if std != 1.0:
+            a *= np.float32(std)
+        if shift != 0.0:
+            a += np.float32(shift)
+        return _to_dtype(a, dt)
+
+    if len(layers) == 1:
+        return one(layers[0]).unsqueeze(0)
+    with ThreadPoolExecutor(_THREADS) as ex:
+        parts = list(ex.map(one, layers))
+    return torch.stack(parts, 0)
+
+
+def make_E(w: Workload, seed: int = 0) -> torch.Tensor:
+    a = normal(seed, "E", 0, (w.T, w.d))
+    if w.outlier_channels:
+        a[:, list(w.outlier_channels)] *= np.float32(w.outlier_scale)
+    return _to_dtype(a, torch_dtype(w))
+
+
+def make_build_weights(w: Workload, seed: int = 0,
+                       layers: Optional[Iterable[int]] = None) -> Dict[str, torch.Tensor]:
+    """Adapter and frozen K/V weights for the requested layers (default: all)."""
+    ls = list(range(w.L)) if layers is None else list(layers)
+    dt = torch_dtype(w)
+    return {
+        "Dw": _per_layer(seed, "Dw", ls, (w.r, w.d), w.d ** -0.5, 0.0, dt),
+        "Uw": _per_layer(seed, "Uw", ls, (w.d, w.r), w.r ** -0.5, 0.0, dt),
+        "gamma": _per_layer(seed, "gamma", ls, (w.d,), 0.1, 1.0, dt),
+        "Wk": _per_layer(seed, "Wk", ls, (w.kv, w.d), w.d ** -0.5, 0.0, dt),
+        "Wv": _per_layer(seed, "Wv", ls, (w.kv, w.d), w.d ** -0.5, 0.0, dt),
+    }
+
+
+def make_text(w: Workload, seed: int = 0,
+              layers: Optional[Iterable[int]] = None) -> Dict[str, torch.Tensor]:
+    """Text queries and text K/V cache for the requested layers."""
+    ls = list(range(w.L)) if layers is None else list(layers)
+    dt = torch_dtype(w)
+    return {
+        "Q": _per_layer(seed, "Q", ls, (w.B, w.Nq, w.Hq, w.hd), 1.0, 0.0, dt),
+        "Kt": _per_layer(seed, "Kt", ls, (w.B, w.Hkv, w.Nkt, w.hd), 1.0, 0.0, dt),
+        "Vt": _per_layer(seed, "Vt", ls, (w.B, w.Hkv, w.Nkt, w.hd), 1.0, 0.0, dt),
+    }
+
+
+def make_visual_cache(w: Workload, seed: int = 0,
+                      layers: Optional[Iterable[int]] = None) -> Dict[str, torch.Tensor]:
+    """Cached visual K/V drawn directly (used where attention is tested alone)."""
+    ls = list(range(w.L)) if layers is None else list(layers)
+    dt = torch_dtype(w)
+    return {
+        "Kv": _per_layer(seed, "Kv", ls, (w.B, w.Hkv, w.Nv, w.hd), 1.0, 0.0, dt),
+        "Vv": _per_layer(seed, "Vv", ls, (w.B, w.Hkv, w.Nv, w.hd), 1.0, 0.0, dt),
+    }
+
+
+def as_f64(t: torch.Tensor) -> np.ndarray:
+    """The exact values a tensor holds, widened to fp64 for the oracle."""
+    return t.detach().to("cpu").to(torch.float64).numpy()
