@@ -1,0 +1,298 @@
+"""Benchmark of the visual-memory path on one MI355X.
+
+A step is one pass of the whole path over one batch: the all-layer down
+projection, the per-layer memories + RMSNorm + visual K/V projection for every
+layer, and the text-query attention of every layer. The default workload is
+the LLaVA-1.5-7B-shaped batch (4 sequences x 576 visual + 64 text tokens, 32
+layers, bf16). Inputs are seeded synthetic tensors already resident in HBM when
+the timed region starts.
+
+Prints one JSON line with the whole-step throughput, a roofline entry for the
+dominant kernel (timed with HIP events around its own launches inside the timed
+region), per-stage figures and a CPU baseline of the fp64 oracle.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "visual tokens/sec (memory build+KV) & text-attn TFLOP/s; % MFMA / HBM peak"
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="llava7b",
+                   choices=["llava7b", "llava_next", "qwen25vl_video", "decode", "tiny"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-decode", action="store_true",
+                   help="skip the decode-shape measurement appended to prefill workloads")
+    return p.parse_args()
+
+
+def cpu_baseline(w, E, wts, tx, vcache):
+    """Time the fp64 oracle on a bounded sample of the same workload and scale it to the step."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2609_34972_amd import configs, synth
+
+    f64 = synth.as_f64
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    tok, nl = 64, min(4, w.L)
+    E64 = f64(E[:tok])
+    li = torch.arange(nl)
+    Dw, Uw, g = f64(wts["Dw"][li]), f64(wts["Uw"][li]), f64(wts["gamma"][li])
+    Wk, Wv = f64(wts["Wk"][li]), f64(wts["Wv"][li])
+    t0 = time.perf_counter()
+    Z = oracle.down(E64, Dw, w.act)
+    oracle.project_visual_kv(E64, Z, Uw, g, Wk, Wv, 1, tok, w.Hkv, w.hd, w.eps)
+    t_build = time.perf_counter() - t0
+    build_per_token = t_build / tok * (w.L / nl)
+    groups = 2
+    t0 = time.perf_counter()
+    for b in range(groups):
+        hs = slice(0, w.G)
+        oracle.text_visual_attention(f64(tx["Q"][0][b:b + 1, :, hs]), f64(vcache["Kv"][0][b:b + 1, :1]),
+                                     f64(vcache["Vv"][0][b:b + 1, :1]), f64(tx["Kt"][0][b:b + 1, :1]),
+                                     f64(tx["Vt"][0][b:b + 1, :1]), w.q_pos0)
+    t_attn = (time.perf_counter() - t0) / groups * (w.B * w.Hkv) * w.L
+    t_step = build_per_token * w.T + t_attn
+    return {
+        "value": w.T / t_step,
+        "unit": "visual tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"fp64 oracle: build+KV of {tok} tokens x {nl} of {w.L} layers "
+                   f"({t_build:.2f} s, scaled x{w.T / tok * w.L / nl:.0f}); attention of "
+                   f"{groups} (batch, kv-head) groups of one layer ({t_attn / (w.B * w.Hkv * w.L) * groups:.2f} s, "
+                   f"scaled x{w.B * w.Hkv * w.L / groups:.0f}); whole step {t_step:.1f} s"),
+    }
+
+
+def run_prefill(args, w):
+    import torch
+
+    import paper_2609_34972_amd as dvl
+    from paper_2609_34972_amd import configs, synth
+
+    dev = torch.device("cuda:0")
+    log(f"[bench] generating {w.name} inputs")
+    E = synth.make_E(w)
+    wts = synth.make_build_weights(w)
+    tx = synth.make_text(w)
+    Eg = E.to(dev)
+    wg = {k: v.to(dev) for k, v in wts.items()}
+    tg = {k: v.to(dev) for k, v in tx.items()}
+    dt = Eg.dtype
+    Z = torch.empty(w.L, w.T, w.r, dtype=dt, device=dev)
+    Kv = torch.empty(w.L, w.B, w.Hkv, w.Nv, w.hd, dtype=dt, device=dev)
+    Vv = torch.empty_like(Kv)
+    O = torch.empty_like(tg["Q"])
+    ws_kv = torch.empty(dvl.project_visual_kv_workspace(w.T, w.d, w.L, dt), dtype=torch.uint8,
+                        device=dev)
+    na = dvl.text_visual_attention_workspace(w.B, w.Hq, w.Hkv, w.hd, w.Nv, w.Nq, w.Nkt)
+    ws_at = torch.empty(max(na, 16), dtype=torch.uint8, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            dvl.time_kernel(dvl.KERNEL_DOWN, *ev["down"])
+            dvl.time_kernel(dvl.KERNEL_UP, *ev["up"])
+            dvl.time_kernel(dvl.KERNEL_KV, *ev["kv"])
+        dvl.build_visual_memory(Eg, wg["Dw"], Z, act=w.act)
+        dvl.project_visual_kv(Eg, Z, wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv, Vv, eps=w.eps,
+                              ws=ws_kv)
+        for l in range(w.L):
+            if ev is not None:
+                dvl.time_kernel(dvl.KERNEL_ATTENTION, *ev["attn"][l])
+            dvl.text_visual_attention(tg["Q"][l], Kv[l], Vv[l], tg["Kt"][l], tg["Vt"][l], O[l],
+                                      q_pos0=w.q_pos0, ws=ws_at)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    evs = [{"down": (mk(), mk()), "up": (mk(), mk()), "kv": (mk(), mk()),
+            "attn": [(mk(), mk()) for _ in range(w.L)]} for _ in range(args.steps)]
+    t_begin, t_end = mk(), mk()
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t_begin.record()
+    for s in range(args.steps):
+        step(evs[s])
+    t_end.record()
+    torch.cuda.synchronize()
+    for k in (dvl.KERNEL_DOWN, dvl.KERNEL_UP, dvl.KERNEL_KV, dvl.KERNEL_ATTENTION):
+        dvl.time_kernel(k)
+    ms_total = t_begin.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    avg = lambda key: sum(e[key][0].elapsed_time(e[key][1]) for e in evs) / args.steps
+    ms_down, ms_up, ms_kv = avg("down"), avg("up"), avg("kv")
+    ms_attn_launch = sum(a[0].elapsed_time(a[1]) for e in evs for a in e["attn"]) / (args.steps * w.L)
+
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    f_down = 2.0 * w.T * w.d * w.r * w.L
+    f_up = 2.0 * w.T * w.r * w.d * w.L
+    f_kv = 2.0 * w.T * 2 * w.kv * w.d * w.L
+    f_build = f_down + f_up + f_kv
+    f_attn = configs.flops_attention(w)
+    b_attn = configs.bytes_attention(w)
+    ms_build = ms_down + ms_up + ms_kv
+    ms_attn_total = ms_step - ms_build
+    kv_tflops = f_kv / (ms_kv * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": w.T / (ms_step * 1e-3),
+        "unit": "visual tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.B, "visual_tokens": w.Nv, "text_tokens": w.Nt,
+                   "layers": w.L, "d": w.d, "rank": w.r, "q_heads": w.Hq, "kv_heads": w.Hkv,
+                   "head_dim": w.hd},
+        "roofline": {"bound": "mfma", "kernel": "k_kv_proj", "achieved": kv_tflops, "peak": peak,
+                     "unit": "TFLOP/s", "frac": kv_tflops / peak, "traffic": None,
+                     "algorithmic_flops_per_launch": f_kv, "ms_per_launch": ms_kv},
+        "stages": {
+            "build_kv_visual_tokens_per_s": w.T / (ms_build * 1e-3),
+            "build_kv_ms": ms_build,
+            "build_kv_tflops": f_build / (ms_build * 1e-3) / 1e12,
+            "build_kv_mfma_frac": f_build / (ms_build * 1e-3) / 1e12 / peak,
+            "down_ms": ms_down, "up_ms": ms_up, "kv_ms": ms_kv,
+            "attention_ms_all_layers": ms_attn_total,
+            "attention_kernel_ms_per_layer": ms_attn_launch,
+            "attention_tflops": f_attn / (ms_attn_total * 1e-3) / 1e12,
+            "attention_gbs": b_attn / (ms_attn_total * 1e-3) / 1e9,
+            "attention_hbm_frac": b_attn / (ms_attn_total * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "step_mfma_frac": (f_build + f_attn) / (ms_step * 1e-3) / 1e12 / peak,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle baseline")
+        vc = synth.make_visual_cache(w, layers=[0])
+        out["cpu_baseline"] = cpu_baseline(w, E, wts, {k: v[:1] for k, v in tx.items()}, vc)
+    del Eg, wg, tg, Z, Kv, Vv, O, ws_kv, ws_at
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_decode(args, w, layers_timed=None):
+    """Decode: one new text token per sequence reading every layer's cached visual and text K/V."""
+    import torch
+
+    import paper_2609_34972_amd as dvl
+    from paper_2609_34972_amd import configs
+
+    dev = torch.device("cuda:0")
+    L = w.L if layers_timed is None else layers_timed
+    log(f"[bench] generating decode caches for {L} layers on the GPU")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    rn = lambda *s: torch.randn(*s, generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    caches = []
+    for _ in range(L):
+        caches.append({"Q": rn(w.B, 1, w.Hq, w.hd), "Kv": rn(w.B, w.Hkv, w.Nv, w.hd),
+                       "Vv": rn(w.B, w.Hkv, w.Nv, w.hd), "Kt": rn(w.B, w.Hkv, w.Nkt, w.hd),
+                       "Vt": rn(w.B, w.Hkv, w.Nkt, w.hd)})
+    O = torch.empty(w.B, 1, w.Hq, w.hd, dtype=torch.bfloat16, device=dev)
+    na = dvl.text_visual_attention_workspace(w.B, w.Hq, w.Hkv, w.hd, w.Nv, 1, w.Nkt)
+    ws = torch.empty(max(na, 16), dtype=torch.uint8, device=dev)
+
+    def step(ev=None):
+        for l in range(L):
+            c = caches[l]
+            if ev is not None:
+                dvl.time_kernel(dvl.KERNEL_ATTENTION, *ev[l])
+            dvl.text_visual_attention(c["Q"], c["Kv"], c["Vv"], c["Kt"], c["Vt"], O, q_pos0=w.q_pos0,
+                                      ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    evs = [[(mk(), mk()) for _ in range(L)] for _ in range(args.steps)]
+    t0, t1 = mk(), mk()
+    t0.record()
+    for s in range(args.steps):
+        step(evs[s])
+    t1.record()
+    torch.cuda.synchronize()
+    dvl.time_kernel(dvl.KERNEL_ATTENTION)
+    ms_step = t0.elapsed_time(t1) / args.steps
+    ms_launch = sum(a.elapsed_time(b) for e in evs for a, b in e) / (args.steps * L)
+    bytes_layer = configs.bytes_attention(w, layers=1)
+    gbs = bytes_layer / (ms_launch * 1e-3) / 1e9
+    res = {"ms_per_step": ms_step, "layers": L, "ms_per_layer": ms_step / L,
+           "kernel_ms_per_layer": ms_launch, "algorithmic_bytes_per_layer": bytes_layer,
+           "kernel_gbs": gbs, "kernel_hbm_frac": gbs / PEAK_HBM_GBS,
+           "step_gbs": bytes_layer * L / (ms_step * 1e-3) / 1e9,
+           "tokens_per_s": w.B / (ms_step * 1e-3)}
+    del caches, O, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported by this build "
+              "(the path runs on a single MI355X; see the sharding notes in the design document)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2609_34972_amd import configs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = configs.get(args.workload)
+    if w.decode:
+        d = run_decode(args, w)
+        out = {
+            "metric": METRIC, "value": d["tokens_per_s"], "unit": "decoded tokens/s (32 layers)",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": d["ms_per_step"],
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic",
+            "config": {"workload": w.name, "batch": w.B, "visual_tokens": w.Nv,
+                       "text_keys": w.Nkt, "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv,
+                       "head_dim": w.hd},
+            "roofline": {"bound": "hbm", "kernel": "k_attn_decode", "achieved": d["kernel_gbs"],
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": d["kernel_hbm_frac"],
+                         "traffic": None,
+                         "algorithmic_bytes_per_launch": d["algorithmic_bytes_per_layer"],
+                         "ms_per_launch": d["kernel_ms_per_layer"]},
+            "decode": d,
+        }
+    else:
+        out = run_prefill(args, w)
+        if not args.no_decode:
+            out["decode"] = run_decode(args, configs.DECODE)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

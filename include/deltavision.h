@@ -1,0 +1,152 @@
+/*
+ * deltavision.h - C ABI of the MI355X (gfx950) visual-memory library.
+ *
+ * The library implements the hot path of delta-Vision ("Just MLPs: Efficient
+ * Visual State Reconstruction for Multimodal Language Models"): per-layer
+ * low-rank adapters build each layer's visual memory from the shared visual
+ * embeddings (Section 3.1, Eq. 4-5), the memory is normalised and projected by
+ * the frozen per-layer key/value weights (Section 3.2, Eq. 7), and text queries
+ * attend over all visual keys plus their own causal text context (Section 3.2,
+ * Eq. 9). Visual tokens never get queries, attention outputs or FFN updates.
+ *
+ * Conventions shared by every call
+ *  - Pointers are DEVICE pointers to dense, row-major tensors in the shapes
+ *    given below, 16-byte aligned. Outputs must not alias inputs.
+ *  - `dtype` (dv_dtype) applies to every tensor of a call, including Z and the
+ *    workspace-backed intermediates. Accumulation is always fp32.
+ *  - Weights are stored out x in, like nn.Linear: Dw[l] = D_l^T [r,d],
+ *    Uw[l] = U_l^T [d,r], Wk[l], Wv[l] [Hkv*hd, d].
+ *  - `stream` is a hipStream_t (NULL = the default stream). Every call only
+ *    enqueues work on it and returns; nothing is synchronised.
+ *  - Ownership: the caller allocates and frees every buffer, including the
+ *    workspace. The library keeps no state besides a thread-local error text
+ *    and the thread-local events of the profiling hook (dv_time_kernel).
+ *  - Errors: arguments are validated on the host before anything is enqueued;
+ *    on error nothing is launched and no output is written. A failed launch
+ *    returns DV_ERR_HIP. No C++ exception crosses this boundary.
+ *  - Supported: dtype f32 or bf16; hd in {64, 128}; Hq % Hkv == 0;
+ *    d % 64 == 0; r % 16 == 0; all sizes > 0 unless stated.
+ */
+#ifndef DELTAVISION_H_
+#define DELTAVISION_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DV_OK = 0,
+  DV_ERR_NULL = 1,        /* a required pointer is NULL */
+  DV_ERR_SHAPE = 2,       /* sizes are negative, zero where not allowed, or inconsistent */
+  DV_ERR_UNSUPPORTED = 3, /* valid but outside the supported set (dtype, act, hd, d, r) */
+  DV_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
+  DV_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the minimum */
+  DV_ERR_HIP = 6,         /* the HIP runtime reported an error while enqueuing */
+  DV_ERR_INTERNAL = 7
+} dv_status;
+
+typedef enum { DV_F32 = 0, DV_BF16 = 1 } dv_dtype;
+
+typedef enum {
+  DV_ACT_SILU = 0, /* phi of Section 3.1 */
+  DV_ACT_GELU = 1  /* x * Phi(x), exact (erf) form */
+} dv_act;
+
+/*
+ * Down half of the adapter (Section 3.1, Eq. 4) for ALL layers at once. The
+ * embedding adapter (Eq. 5) feeds every layer the same E, so the per-layer
+ * products E D_l form one GEMM of E against [D_0 | ... | D_{L-1}]:
+ *     Z[l][t][j] = phi( sum_k E[t][k] * Dw[l][j][k] ),   l < L, t < T, j < r.
+ *   E  [T, d]     visual embeddings (Section 2, Eq. 1), T = batch * visual tokens
+ *   Dw [L, r, d]  down-projections, out x in
+ *   Z  [L, T, r]  output (dtype of the call), phi applied in fp32 before rounding
+ *   act           dv_act
+ */
+dv_status dv_build_visual_memory(const void* E, const void* Dw, void* Z, int64_t T, int32_t d,
+                                 int32_t L, int32_t r, int32_t act, int32_t dtype, void* stream);
+
+/*
+ * Up half of the adapter (Eq. 4-5) and the visual key/value projection
+ * (Section 3.2, Eq. 7) for layers l0 <= l < l0 + nl:
+ *     M_l  = E + Z_l U_l                       (memory of layer l)
+ *     N_l  = M_l * rsqrt(mean_k M_l^2 + eps) * gamma_l   (LN_l read as RMSNorm)
+ *     Kv_l = N_l Wk[l]^T,  Vv_l = N_l Wv[l]^T, stored head-major
+ *   E     [B*Nv, d]
+ *   Z     [L, B*Nv, r]   from dv_build_visual_memory
+ *   Uw    [L, d, r]      up-projections, out x in
+ *   gamma [L, d]         frozen RMSNorm weights
+ *   Wk,Wv [L, Hkv*hd, d] frozen key / value projections
+ *   Kv,Vv [L, B, Hkv, Nv, hd] outputs; only the slots of layers l0..l0+nl-1 are written
+ *   ws    workspace; at least dv_project_visual_kv_workspace(B*Nv, d, 1, dtype) bytes.
+ *         With room for k layers the call processes layers in groups of up to k;
+ *         dv_project_visual_kv_workspace(B*Nv, d, nl, dtype) holds all of them at once.
+ * M_l is transient (it lives only in the workspace), as the method prescribes.
+ */
+size_t dv_project_visual_kv_workspace(int64_t T, int32_t d, int32_t nl, int32_t dtype);
+dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
+                               const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
+                               int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
+                               int32_t hd, int32_t l0, int32_t nl, float eps, int32_t dtype,
+                               void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Text-query attention of one layer over [visual; text] keys (Section 3.2,
+ * Eq. 9; visual tokens precede the text, Section 2 Eq. 2):
+ *     O[b,i,h,:] = sum_j softmax_j( scale * <Q[b,i,h,:], K_j> ) V_j
+ * over every visual key j < Nv of kv-head g = h / (Hq/Hkv) and the text keys
+ * 0..q_pos0+i of the same head (causal). Prefill: q_pos0 = 0, Nq = Nkt. Decode:
+ * Nq = 1 and q_pos0 = number of earlier text tokens (the new token's key is
+ * text key q_pos0). Nv may be 0 (visual read blocked).
+ *   Q, O   [B, Nq, Hq, hd]
+ *   Kv, Vv [B, Hkv, Nv, hd]   one layer of the visual cache (may be NULL when Nv == 0)
+ *   Kt, Vt [B, Hkv, Nkt, hd]  text key / value cache; requires q_pos0 + Nq <= Nkt
+ *   scale  softmax scale, usually 1/sqrt(hd)
+ *   ws     split-key partials; may be NULL/0 (then keys are not split). With
+ *          dv_text_visual_attention_workspace(...) bytes the call picks its
+ *          preferred split; with fewer it uses the largest split that fits.
+ */
+size_t dv_text_visual_attention_workspace(int32_t B, int32_t Hq, int32_t Hkv, int32_t hd,
+                                          int32_t Nv, int32_t Nq, int32_t Nkt);
+dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv, const void* Kt,
+                                   const void* Vt, void* O, int32_t B, int32_t Hq, int32_t Hkv,
+                                   int32_t hd, int32_t Nv, int32_t Nq, int32_t Nkt,
+                                   int32_t q_pos0, float scale, int32_t dtype, void* ws,
+                                   size_t ws_bytes, void* stream);
+
+/*
+ * Profiling hook. Kernels of the library, as named by dv_kernel:
+ *   DV_KERNEL_DOWN       the all-layer down-projection of dv_build_visual_memory
+ *   DV_KERNEL_UP         the up-projection + residual of dv_project_visual_kv
+ *   DV_KERNEL_KV         the RMSNorm-scaled K/V projection of dv_project_visual_kv
+ *   DV_KERNEL_ATTENTION  the main attention kernel of dv_text_visual_attention
+ *                        (without the split-merge kernel)
+ * After dv_time_kernel(k, begin, end) with two hipEvent_t handles, every launch
+ * of kernel k made by later calls on this thread is bracketed by
+ * hipEventRecord(begin) and hipEventRecord(end) on the call's stream; when a
+ * call launches k several times (a projection in layer groups) the pair spans
+ * the first to the last launch. NULL, NULL switches the hook off. The events
+ * stay owned by the caller and must outlive the calls that record them.
+ */
+typedef enum {
+  DV_KERNEL_DOWN = 0,
+  DV_KERNEL_UP = 1,
+  DV_KERNEL_KV = 2,
+  DV_KERNEL_ATTENTION = 3
+} dv_kernel;
+dv_status dv_time_kernel(int32_t kernel, void* ev_begin, void* ev_end);
+
+/* Human-readable name of a status code (static storage). */
+const char* dv_status_string(int32_t status);
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char* dv_last_error(void);
+/* ABI version, incremented on any incompatible change. */
+int32_t dv_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DELTAVISION_H_ */

@@ -1,0 +1,20 @@
+"""delta-Vision visual-memory path for MI355X (gfx950).
+
+Per-layer low-rank adapters build each layer's visual memory from the shared
+visual embeddings (Section 3.1, Eq. 4-5), the memory is normalised and
+projected by the frozen per-layer K/V weights (Section 3.2, Eq. 7), and text
+queries attend over all visual keys plus their own causal context (Section 3.2,
+Eq. 9). The arithmetic runs in hand-written HIP kernels behind the C ABI of
+``include/deltavision.h``; this package only marshals tensors into it.
+"""
+from ._lib import (ACT_GELU, ACT_SILU, KERNEL_ATTENTION, KERNEL_DOWN, KERNEL_KV, KERNEL_UP,
+                   DeltaVisionError, build_visual_memory, load, project_visual_kv,
+                   project_visual_kv_workspace, text_visual_attention,
+                   text_visual_attention_workspace, time_kernel)
+
+__all__ = [
+    "ACT_SILU", "ACT_GELU", "DeltaVisionError", "load", "build_visual_memory",
+    "project_visual_kv", "project_visual_kv_workspace", "text_visual_attention",
+    "text_visual_attention_workspace", "time_kernel", "KERNEL_DOWN", "KERNEL_UP", "KERNEL_KV",
+    "KERNEL_ATTENTION",
+]

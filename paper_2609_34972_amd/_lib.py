@@ -1,0 +1,193 @@
+"""Python binding of ``libdeltavision.so``: argument marshalling only.
+
+Every function takes torch tensors that live in device memory, derives the
+sizes the C ABI expects from their shapes, passes raw device pointers and the
+current HIP stream, and raises on a non-zero status. All arithmetic happens in
+the library's gfx950 kernels; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdeltavision.so")
+
+DV_F32, DV_BF16 = 0, 1
+ACT_SILU, ACT_GELU = 0, 1
+
+# Every symbol declared by include/deltavision.h.
+EXPORTS = (
+    "dv_build_visual_memory",
+    "dv_project_visual_kv_workspace",
+    "dv_project_visual_kv",
+    "dv_text_visual_attention_workspace",
+    "dv_text_visual_attention",
+    "dv_status_string",
+    "dv_last_error",
+    "dv_abi_version",
+    "dv_time_kernel",
+)
+
+KERNEL_DOWN, KERNEL_UP, KERNEL_KV, KERNEL_ATTENTION = 0, 1, 2, 3
+
+_lock = threading.Lock()
+_lib = None
+
+
+class DeltaVisionError(RuntimeError):
+    def __init__(self, status: int, name: str, detail: str):
+        super().__init__(f"{name}: {detail}" if detail else name)
+        self.status = status
+        self.name = name
+
+
+def load() -> ctypes.CDLL:
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2609_34972_amd.build` "
+                "(or __graft_entry__.build()); there is no non-HIP implementation")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+        lib.dv_build_visual_memory.argtypes = [vp, vp, vp, i64, i32, i32, i32, i32, i32, vp]
+        lib.dv_build_visual_memory.restype = i32
+        lib.dv_project_visual_kv_workspace.argtypes = [i64, i32, i32, i32]
+        lib.dv_project_visual_kv_workspace.restype = sz
+        lib.dv_project_visual_kv.argtypes = [vp] * 8 + [i32] * 9 + [f32, i32, vp, sz, vp]
+        lib.dv_project_visual_kv.restype = i32
+        lib.dv_text_visual_attention_workspace.argtypes = [i32] * 7
+        lib.dv_text_visual_attention_workspace.restype = sz
+        lib.dv_text_visual_attention.argtypes = [vp] * 6 + [i32] * 8 + [f32, i32, vp, sz, vp]
+        lib.dv_text_visual_attention.restype = i32
+        lib.dv_status_string.argtypes = [i32]
+        lib.dv_status_string.restype = ctypes.c_char_p
+        lib.dv_last_error.argtypes = []
+        lib.dv_last_error.restype = ctypes.c_char_p
+        lib.dv_abi_version.argtypes = []
+        lib.dv_abi_version.restype = i32
+        lib.dv_time_kernel.argtypes = [i32, vp, vp]
+        lib.dv_time_kernel.restype = i32
+        _lib = lib
+        return lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        lib = load()
+        raise DeltaVisionError(status, lib.dv_status_string(status).decode(),
+                               lib.dv_last_error().decode())
+
+
+def _dtype_code(*ts: torch.Tensor) -> int:
+    dt = ts[0].dtype
+    for t in ts:
+        if t.dtype != dt:
+            raise TypeError(f"all tensors of a call must share one dtype ({t.dtype} vs {dt})")
+    if dt == torch.bfloat16:
+        return DV_BF16
+    if dt == torch.float32:
+        return DV_F32
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must be in device memory")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(device: torch.device, stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return s.cuda_stream
+
+
+def time_kernel(kernel: int, begin=None, end=None) -> None:
+    """Bracket every later launch of `kernel` on this thread with two torch.cuda.Event
+    (created with enable_timing=True); time_kernel(kernel) switches the hook off."""
+    b = begin.cuda_event if begin is not None else None
+    e = end.cuda_event if end is not None else None
+    _check(load().dv_time_kernel(kernel, b, e))
+
+
+def build_visual_memory(E: torch.Tensor, Dw: torch.Tensor, Z: torch.Tensor, act: int = ACT_SILU,
+                        stream=None) -> torch.Tensor:
+    """Z[l] = phi(E D_l) for every layer. E [T,d], Dw [L,r,d], Z [L,T,r]."""
+    T, d = E.shape
+    L, r, d2 = Dw.shape
+    if d2 != d or tuple(Z.shape) != (L, T, r):
+        raise ValueError(f"shape mismatch: E {tuple(E.shape)} Dw {tuple(Dw.shape)} Z {tuple(Z.shape)}")
+    code = _dtype_code(E, Dw, Z)
+    _check(load().dv_build_visual_memory(_ptr(E), _ptr(Dw), _ptr(Z), T, d, L, r, act, code,
+                                         _stream(E.device, stream)))
+    return Z
+
+
+def project_visual_kv_workspace(T: int, d: int, nl: int, dtype: torch.dtype) -> int:
+    code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
+    return int(load().dv_project_visual_kv_workspace(T, d, nl, code))
+
+
+def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, l0: int = 0,
+                      nl: Optional[int] = None, ws: Optional[torch.Tensor] = None, stream=None):
+    """Memories, RMSNorm and visual K/V of layers l0..l0+nl-1 into Kv, Vv [L,B,Hkv,Nv,hd]."""
+    L, B, Hkv, Nv, hd = Kv.shape
+    T, d = E.shape
+    r = Z.shape[2]
+    if nl is None:
+        nl = L - l0
+    if (T != B * Nv or tuple(Z.shape) != (L, T, r) or tuple(Uw.shape) != (L, d, r)
+            or tuple(gamma.shape) != (L, d) or tuple(Wk.shape) != (L, Hkv * hd, d)
+            or Wv.shape != Wk.shape or Vv.shape != Kv.shape):
+        raise ValueError("shape mismatch in project_visual_kv")
+    code = _dtype_code(E, Z, Uw, gamma, Wk, Wv, Kv, Vv)
+    if ws is None:
+        ws = torch.empty(project_visual_kv_workspace(T, d, nl, E.dtype), dtype=torch.uint8,
+                         device=E.device)
+    _check(load().dv_project_visual_kv(_ptr(E), _ptr(Z), _ptr(Uw), _ptr(gamma), _ptr(Wk), _ptr(Wv),
+                                       _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, l0, nl,
+                                       float(eps), code, _ptr(ws), ws.numel(),
+                                       _stream(E.device, stream)))
+    return Kv, Vv
+
+
+def text_visual_attention_workspace(B: int, Hq: int, Hkv: int, hd: int, Nv: int, Nq: int,
+                                    Nkt: int) -> int:
+    return int(load().dv_text_visual_attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nkt))
+
+
+def text_visual_attention(Q, Kv, Vv, Kt, Vt, O, q_pos0: int = 0, scale: Optional[float] = None,
+                          ws: Optional[torch.Tensor] = None, stream=None):
+    """One layer of Eq. 9. Q, O [B,Nq,Hq,hd]; Kv, Vv [B,Hkv,Nv,hd]; Kt, Vt [B,Hkv,Nkt,hd]."""
+    B, Nq, Hq, hd = Q.shape
+    _, Hkv, Nkt, _ = Kt.shape
+    Nv = Kv.shape[2]
+    if (tuple(Kv.shape) != (B, Hkv, Nv, hd) or Vv.shape != Kv.shape or Vt.shape != Kt.shape
+            or Kt.shape[0] != B or Kt.shape[3] != hd or O.shape != Q.shape):
+        raise ValueError("shape mismatch in text_visual_attention")
+    code = _dtype_code(Q, Kv, Vv, Kt, Vt, O)
+    if scale is None:
+        scale = hd ** -0.5
+    if ws is None:
+        n = text_visual_attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nkt)
+        ws = torch.empty(max(n, 16), dtype=torch.uint8, device=Q.device) if n else None
+    kvp = _ptr(Kv) if Nv > 0 else None
+    vvp = _ptr(Vv) if Nv > 0 else None
+    _check(load().dv_text_visual_attention(_ptr(Q), kvp, vvp, _ptr(Kt), _ptr(Vt), _ptr(O), B, Hq,
+                                           Hkv, hd, Nv, Nq, Nkt, q_pos0, float(scale), code,
+                                           _ptr(ws) if ws is not None else None,
+                                           ws.numel() if ws is not None else 0,
+                                           _stream(Q.device, stream)))
+    return O

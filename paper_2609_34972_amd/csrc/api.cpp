@@ -1,0 +1,248 @@
+// C ABI of the visual-memory library: argument validation, workspace layout
+// and dispatch to the gfx950 kernels. Every check runs on the host before
+// anything is enqueued, so a rejected call launches nothing and writes nothing.
+#include "../../include/deltavision.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "attention.hpp"
+#include "build_kernels.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+thread_local dv::LaunchEvents g_ev;
+
+dv_status fail(dv_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+dv_status ok() {
+  g_err[0] = '\0';
+  return DV_OK;
+}
+
+// Token rows per call: the row-tile index of the GEMM kernels is a 16-bit grid
+// dimension (65535 tiles of 64 rows).
+constexpr int64_t kMaxTokens = 65535LL * 64;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t elem_size(int32_t dtype) { return dtype == DV_BF16 ? 2 : 4; }
+
+dv_status check_dtype(int32_t dtype) {
+  if (dtype != DV_F32 && dtype != DV_BF16)
+    return fail(DV_ERR_UNSUPPORTED, "dtype %d is not DV_F32 or DV_BF16", dtype);
+  return DV_OK;
+}
+
+#define DV_CHECK(expr)              \
+  do {                              \
+    dv_status s_ = (expr);          \
+    if (s_ != DV_OK) return s_;     \
+  } while (0)
+
+dv_status need_ptr(const void* p, const char* name) {
+  if (!p) return fail(DV_ERR_NULL, "%s is NULL", name);
+  if (!aligned16(p)) return fail(DV_ERR_ALIGN, "%s is not 16-byte aligned", name);
+  return DV_OK;
+}
+
+dv_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(DV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+// Bytes of one layer's slot in the projection workspace: the gamma-weighted
+// memory in the call dtype, then the fp32 partial sums of squares.
+size_t kv_ws_layer_bytes(int64_t T, int32_t d, int32_t dtype) {
+  const size_t mem = (size_t)T * (size_t)d * elem_size(dtype);
+  const size_t mem_al = (mem + 255) / 256 * 256;
+  const size_t ssq = (size_t)dv::kv_partials(d, dtype == DV_BF16 ? 1 : 0) * (size_t)T * 4;
+  return mem_al + (ssq + 255) / 256 * 256;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t dv_abi_version(void) { return 1; }
+
+const char* dv_status_string(int32_t status) {
+  switch (status) {
+    case DV_OK: return "DV_OK";
+    case DV_ERR_NULL: return "DV_ERR_NULL";
+    case DV_ERR_SHAPE: return "DV_ERR_SHAPE";
+    case DV_ERR_UNSUPPORTED: return "DV_ERR_UNSUPPORTED";
+    case DV_ERR_ALIGN: return "DV_ERR_ALIGN";
+    case DV_ERR_WORKSPACE: return "DV_ERR_WORKSPACE";
+    case DV_ERR_HIP: return "DV_ERR_HIP";
+    case DV_ERR_INTERNAL: return "DV_ERR_INTERNAL";
+    default: return "DV_UNKNOWN_STATUS";
+  }
+}
+
+const char* dv_last_error(void) { return g_err; }
+
+dv_status dv_time_kernel(int32_t kernel, void* ev_begin, void* ev_end) {
+  if ((ev_begin == nullptr) != (ev_end == nullptr))
+    return fail(DV_ERR_NULL, "dv_time_kernel needs both events or neither");
+  hipEvent_t* slot = nullptr;
+  switch (kernel) {
+    case DV_KERNEL_DOWN: slot = g_ev.down; break;
+    case DV_KERNEL_UP: slot = g_ev.up; break;
+    case DV_KERNEL_KV: slot = g_ev.kv; break;
+    case DV_KERNEL_ATTENTION: slot = g_ev.attn; break;
+    default: return fail(DV_ERR_UNSUPPORTED, "unknown kernel id %d", kernel);
+  }
+  slot[0] = (hipEvent_t)ev_begin;
+  slot[1] = (hipEvent_t)ev_end;
+  return ok();
+}
+
+dv_status dv_build_visual_memory(const void* E, const void* Dw, void* Z, int64_t T, int32_t d,
+                                 int32_t L, int32_t r, int32_t act, int32_t dtype, void* stream) {
+  DV_CHECK(check_dtype(dtype));
+  if (T <= 0 || d <= 0 || L <= 0 || r <= 0)
+    return fail(DV_ERR_SHAPE, "sizes must be positive (T=%lld d=%d L=%d r=%d)", (long long)T, d, L, r);
+  if (T > kMaxTokens || (int64_t)L * r > INT32_MAX)
+    return fail(DV_ERR_SHAPE, "T=%lld exceeds %lld or L*r=%lld exceeds 2^31-1", (long long)T,
+                (long long)kMaxTokens, (long long)L * r);
+  if (d % 64 != 0) return fail(DV_ERR_UNSUPPORTED, "d=%d must be a multiple of 64", d);
+  if (r % 16 != 0) return fail(DV_ERR_UNSUPPORTED, "r=%d must be a multiple of 16", r);
+  if (act != DV_ACT_SILU && act != DV_ACT_GELU)
+    return fail(DV_ERR_UNSUPPORTED, "act=%d is not DV_ACT_SILU or DV_ACT_GELU", act);
+  DV_CHECK(need_ptr(E, "E"));
+  DV_CHECK(need_ptr(Dw, "Dw"));
+  DV_CHECK(need_ptr(Z, "Z"));
+  return hip_status(dv::launch_down_act(E, Dw, Z, T, d, L, r, act, dtype == DV_BF16 ? 1 : 0,
+                                        (hipStream_t)stream, g_ev),
+                    "dv_build_visual_memory launch");
+}
+
+size_t dv_project_visual_kv_workspace(int64_t T, int32_t d, int32_t nl, int32_t dtype) {
+  if (T <= 0 || d <= 0 || nl <= 0 || (dtype != DV_F32 && dtype != DV_BF16)) return 0;
+  return (size_t)nl * kv_ws_layer_bytes(T, d, dtype);
+}
+
+dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
+                               const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
+                               int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
+                               int32_t hd, int32_t l0, int32_t nl, float eps, int32_t dtype,
+                               void* ws, size_t ws_bytes, void* stream) {
+  DV_CHECK(check_dtype(dtype));
+  if (B <= 0 || Nv <= 0 || d <= 0 || L <= 0 || r <= 0 || Hkv <= 0 || hd <= 0)
+    return fail(DV_ERR_SHAPE, "sizes must be positive (B=%d Nv=%d d=%d L=%d r=%d Hkv=%d hd=%d)", B,
+                Nv, d, L, r, Hkv, hd);
+  if (l0 < 0 || nl <= 0 || l0 + nl > L)
+    return fail(DV_ERR_SHAPE, "layer range [%d, %d) is not inside [0, %d)", l0, l0 + nl, L);
+  const int64_t T = (int64_t)B * Nv;
+  if (T > kMaxTokens || (int64_t)2 * Hkv * hd > INT32_MAX || nl > 65535)
+    return fail(DV_ERR_SHAPE, "B*Nv=%lld exceeds %lld (or nl > 65535)", (long long)T,
+                (long long)kMaxTokens);
+  if (d % 64 != 0) return fail(DV_ERR_UNSUPPORTED, "d=%d must be a multiple of 64", d);
+  if (r % 16 != 0) return fail(DV_ERR_UNSUPPORTED, "r=%d must be a multiple of 16", r);
+  if (hd != 64 && hd != 128) return fail(DV_ERR_UNSUPPORTED, "hd=%d must be 64 or 128", hd);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(DV_ERR_SHAPE, "eps must be finite and >= 0");
+  DV_CHECK(need_ptr(E, "E"));
+  DV_CHECK(need_ptr(Z, "Z"));
+  DV_CHECK(need_ptr(Uw, "Uw"));
+  DV_CHECK(need_ptr(gamma, "gamma"));
+  DV_CHECK(need_ptr(Wk, "Wk"));
+  DV_CHECK(need_ptr(Wv, "Wv"));
+  DV_CHECK(need_ptr(Kv, "Kv"));
+  DV_CHECK(need_ptr(Vv, "Vv"));
+  const size_t per_layer = kv_ws_layer_bytes(T, d, dtype);
+  if (!ws || ws_bytes < per_layer)
+    return fail(DV_ERR_WORKSPACE, "workspace of %zu bytes is below the one-layer minimum %zu",
+                ws ? ws_bytes : (size_t)0, per_layer);
+  if (!aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
+  const int group = (int)std::min<size_t>((size_t)nl, ws_bytes / per_layer);
+  const size_t mem_al = ((size_t)T * d * elem_size(dtype) + 255) / 256 * 256;
+  for (int g0 = 0; g0 < nl; g0 += group) {
+    const int gl = std::min(group, nl - g0);
+    char* base = (char*)ws;
+    void* Mg = base;
+    float* ssq = (float*)(base + (size_t)gl * mem_al);
+    hipError_t e = dv::launch_project_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B, Nv, d, r, Hkv, hd,
+                                         l0 + g0, gl, eps, dtype == DV_BF16 ? 1 : 0, Mg, ssq,
+                                         (hipStream_t)stream, g_ev, g0 == 0, g0 + gl >= nl);
+    if (e != hipSuccess) return hip_status(e, "dv_project_visual_kv launch");
+  }
+  return ok();
+}
+
+size_t dv_text_visual_attention_workspace(int32_t B, int32_t Hq, int32_t Hkv, int32_t hd,
+                                          int32_t Nv, int32_t Nq, int32_t Nkt) {
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || (hd != 64 && hd != 128) || Nv < 0 ||
+      Nq <= 0 || Nkt < Nq)
+    return 0;
+  return dv::attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nkt);
+}
+
+dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv, const void* Kt,
+                                   const void* Vt, void* O, int32_t B, int32_t Hq, int32_t Hkv,
+                                   int32_t hd, int32_t Nv, int32_t Nq, int32_t Nkt,
+                                   int32_t q_pos0, float scale, int32_t dtype, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  DV_CHECK(check_dtype(dtype));
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || hd <= 0 || Nv < 0 || Nq <= 0 || Nkt <= 0 || q_pos0 < 0)
+    return fail(DV_ERR_SHAPE,
+                "sizes must be positive (B=%d Hq=%d Hkv=%d hd=%d Nq=%d Nkt=%d), Nv and q_pos0 >= 0 "
+                "(Nv=%d q_pos0=%d)", B, Hq, Hkv, hd, Nq, Nkt, Nv, q_pos0);
+  if (Hq % Hkv != 0) return fail(DV_ERR_SHAPE, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
+  if ((int64_t)q_pos0 + Nq > Nkt)
+    return fail(DV_ERR_SHAPE, "q_pos0 + Nq = %lld exceeds the %d text keys",
+                (long long)q_pos0 + Nq, Nkt);
+  if ((int64_t)Nv + Nkt > INT32_MAX / 2 || (int64_t)B * Nq * Hq > INT32_MAX / 256)
+    return fail(DV_ERR_SHAPE, "key count exceeds 2^30 or B*Nq*Hq exceeds 2^23");
+  if ((int64_t)B * Hkv > 65535) return fail(DV_ERR_SHAPE, "B*Hkv=%lld exceeds 65535", (long long)B * Hkv);
+  if (hd != 64 && hd != 128) return fail(DV_ERR_UNSUPPORTED, "hd=%d must be 64 or 128", hd);
+  if (!std::isfinite(scale)) return fail(DV_ERR_SHAPE, "scale must be finite");
+  DV_CHECK(need_ptr(Q, "Q"));
+  if (Nv > 0) {
+    DV_CHECK(need_ptr(Kv, "Kv"));
+    DV_CHECK(need_ptr(Vv, "Vv"));
+  }
+  DV_CHECK(need_ptr(Kt, "Kt"));
+  DV_CHECK(need_ptr(Vt, "Vt"));
+  DV_CHECK(need_ptr(O, "O"));
+  if (ws && !aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
+  const dv::AttnPlan plan =
+      dv::plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, ws ? ws_bytes : 0);
+  dv::AttnArgs a{};
+  a.Q = Q;
+  a.Kv = Kv;
+  a.Vv = Vv;
+  a.Kt = Kt;
+  a.Vt = Vt;
+  a.O = O;
+  const int64_t rows = (int64_t)B * Nq * Hq;
+  a.Opart = (float*)ws;
+  a.MLpart = ws ? (float*)((char*)ws + (size_t)plan.splits * rows * hd * 4) : nullptr;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.hd = hd;
+  a.Nv = Nv;
+  a.Nq = Nq;
+  a.Nkt = Nkt;
+  a.q_pos0 = q_pos0;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.splits = plan.splits;
+  a.keys_per_split = plan.keys_per_split;
+  return hip_status(dv::launch_attention(a, plan, dtype == DV_BF16 ? 1 : 0, (hipStream_t)stream,
+                                         g_ev),
+                    "dv_text_visual_attention launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,527 @@
+// Text-query attention over [visual; text] keys on gfx950 (Section 3.2, Eq. 9).
+//
+// Every text query reads all Nv visual keys of its kv-head and the text keys up
+// to its own position (visual tokens precede the text, Section 2 Eq. 2).
+//
+//   k_attn_prefill  MFMA flash attention. Query rows of one kv-head group are
+//                   packed (row = query * G + head-in-group) so GQA heads share
+//                   each K/V tile. Scores are formed transposed, S^T = K Q^T,
+//                   and the output as O^T = V^T P^T: the accumulator layout then
+//                   keeps one query per lane, so the running max / sum and the
+//                   rescale of O are per-lane and P feeds the second product
+//                   straight from registers. K/V tiles stream through padded
+//                   LDS rows (conflict-free for both access patterns).
+//   k_attn_decode   one query per sequence: a bandwidth-bound stream over the
+//                   K/V caches with 16-byte loads, dot products reduced across
+//                   the lanes of one key row, and an online softmax.
+//   k_attn_combine  log-sum-exp merge of key-split partials.
+#include "attention.hpp"
+#include "dv_device.hpp"
+
+#include <math.h>
+
+namespace dv {
+
+constexpr float NEG_BIG = -1e30f;  // finite start value of the running max
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
+
+template <typename T, int HD, int NW>
+struct AttnCfg {
+  static constexpr int NKB = sizeof(T) == 2 ? 2 : 1;  // 32-key sub-tiles per tile
+  static constexpr int KT = 32 * NKB;              // keys per tile (LDS stays below 64 KiB)
+  static constexpr int NT = NW * WAVE;
+  static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
+  static constexpr int PITCH = HD + EPC;           // LDS row pitch: 16-byte pad per row
+  static constexpr int CPR = HD / EPC;             // chunks per K/V row
+  static constexpr int LD_IT = KT * CPR / NT;      // chunks per thread per tile and tensor
+  static constexpr int KS = HD / 16;               // 16-deep K steps of S^T = K Q^T
+  static constexpr int CB = HD / 32;               // 32-row blocks of O^T
+  static constexpr int LDS_BYTES = 2 * KT * PITCH * (int)sizeof(T);
+  static_assert((KT * CPR) % NT == 0, "tile chunks must divide threads");
+};
+
+template <typename T>
+__device__ __forceinline__ typename Frag8<T>::type lds_row8(const T* s);
+template <>
+__device__ __forceinline__ bf16x8 lds_row8<bf16>(const bf16* s) {
+  return __builtin_bit_cast(bf16x8, ld16(s));
+}
+template <>
+__device__ __forceinline__ f32x8 lds_row8<float>(const float* s) {
+  f32x4 a = __builtin_bit_cast(f32x4, ld16(s)), b = __builtin_bit_cast(f32x4, ld16(s + 4));
+  return f32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+template <typename T>
+__device__ __forceinline__ void load_row8_f32(const T* p, float (&x)[8]);
+template <>
+__device__ __forceinline__ void load_row8_f32<bf16>(const bf16* p, float (&x)[8]) {
+  bf16x8 v = __builtin_bit_cast(bf16x8, ld16(p));
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = (float)v[e];
+}
+template <>
+__device__ __forceinline__ void load_row8_f32<float>(const float* p, float (&x)[8]) {
+  f32x4 a = __builtin_bit_cast(f32x4, ld16(p)), b = __builtin_bit_cast(f32x4, ld16(p + 4));
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[e] = a[e];
+    x[4 + e] = b[e];
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store4(T* p, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void store4<bf16>(bf16* p, float a, float b, float c, float d) {
+  bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
+  *(u32x2*)p = __builtin_bit_cast(u32x2, v);
+}
+template <>
+__device__ __forceinline__ void store4<float>(float* p, float a, float b, float c, float d) {
+  *(f32x4*)p = f32x4{a, b, c, d};
+}
+
+// ------------------------------------------------------------------ prefill
+
+template <typename T, int HD, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn_prefill(AttnArgs a) {
+  typedef AttnCfg<T, HD, NW> C;
+  typedef typename Frag8<T>::type Fr;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* sk = (T*)smem;
+  T* sv = sk + C::KT * C::PITCH;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g2 = lane >> 5;
+  const int G = a.Hq / a.Hkv, R = a.Nq * G;
+  const int bg = blockIdx.y, b = bg / a.Hkv, g = bg - b * a.Hkv;
+  const int split = blockIdx.z;
+
+  // Rows of this block / wave. Row r <-> query i = r / G, head h = g*G + r % G.
+  const int row0 = blockIdx.x * (32 * NW);
+  const int my_row = row0 + wave * 32 + (lane & 31);
+  const bool row_ok = my_row < R;
+  const int my_i = row_ok ? my_row / G : 0;
+  const int my_h = g * G + (row_ok ? my_row - my_i * G : 0);
+  const int last_row = min(row0 + 32 * NW, R) - 1;
+  const int i_max = last_row / G;
+
+  // Key range: this split's slice of [visual; text] cut at the furthest causal limit.
+  const int nk_all = a.Nv + a.q_pos0 + i_max + 1;
+  const int k_begin = split * a.keys_per_split;
+  const int k_end = min(nk_all, k_begin + a.keys_per_split);
+
+  const T* Kvb = (const T*)a.Kv + (int64_t)bg * a.Nv * HD;
+  const T* Vvb = (const T*)a.Vv + (int64_t)bg * a.Nv * HD;
+  const T* Ktb = (const T*)a.Kt + (int64_t)bg * a.Nkt * HD;
+  const T* Vtb = (const T*)a.Vt + (int64_t)bg * a.Nkt * HD;
+
+  // Q^T fragments of this lane's row (B operand), pre-scaled by scale*log2(e).
+  Fr qf[C::KS];
+  {
+    const T* qrow = (const T*)a.Q + (((int64_t)b * a.Nq + my_i) * a.Hq + my_h) * HD;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      float x[8];
+      if (row_ok) load_row8_f32<T>(qrow + ks * 16 + g2 * 8, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[ks][e] = from_f32<T>(row_ok ? x[e] : 0.f);
+    }
+  }
+  const float qscale = a.scale_log2;
+
+  f32x16 oacc[C::CB];
+#pragma unroll
+  for (int cb = 0; cb < C::CB; ++cb) oacc[cb] = f32x16{};
+  float m_run = NEG_BIG, l_run = 0.f;
+  const int my_text_lim = a.Nv + a.q_pos0 + my_i;  // last allowed key index for my row
+
+  u32x4 rk[C::LD_IT], rv[C::LD_IT];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int it = 0; it < C::LD_IT; ++it) {
+      const int idx = tid + it * C::NT, key = idx / C::CPR, ch = idx - key * C::CPR;
+      const int j = k0 + key;
+      if (j < k_end) {
+        const T* ks_ = j < a.Nv ? Kvb + (int64_t)j * HD : Ktb + (int64_t)(j - a.Nv) * HD;
+        const T* vs_ = j < a.Nv ? Vvb + (int64_t)j * HD : Vtb + (int64_t)(j - a.Nv) * HD;
+        rk[it] = ld16(ks_ + ch * C::EPC);
+        rv[it] = ld16(vs_ + ch * C::EPC);
+      } else {
+        rk[it] = u32x4{0, 0, 0, 0};
+        rv[it] = u32x4{0, 0, 0, 0};
+      }
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int it = 0; it < C::LD_IT; ++it) {
+      const int idx = tid + it * C::NT, key = idx / C::CPR, ch = idx - key * C::CPR;
+      *(u32x4*)(sk + key * C::PITCH + ch * C::EPC) = rk[it];
+      *(u32x4*)(sv + key * C::PITCH + ch * C::EPC) = rv[it];
+    }
+  };
+
+  if (k_begin < k_end) gload(k_begin);
+  for (int k0 = k_begin; k0 < k_end; k0 += C::KT) {
+    __syncthreads();  // previous tile fully consumed
+    sstore();
+    __syncthreads();
+    if (k0 + C::KT < k_end) gload(k0 + C::KT);
+
+    // S^T (keys x my queries), one accumulator per 32-key sub-tile.
+    f32x16 sacc[C::NKB];
+#pragma unroll
+    for (int kb = 0; kb < C::NKB; ++kb) {
+      sacc[kb] = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        Fr kf = lds_row8<T>(sk + (kb * 32 + (lane & 31)) * C::PITCH + ks * 16 + g2 * 8);
+        mfma_k16(sacc[kb], kf, qf[ks]);
+      }
+    }
+    // Mask, scale and the running max of my query (shared by the two lane halves).
+    float tmax = NEG_BIG;
+#pragma unroll
+    for (int kb = 0; kb < C::NKB; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int j = k0 + kb * 32 + acc_row(lane, i);
+        const bool ok = j < k_end && j <= my_text_lim;
+        const float s = ok ? sacc[kb][i] * qscale : -INFINITY;
+        sacc[kb][i] = s;
+        tmax = fmaxf(tmax, s);
+      }
+    tmax = fmaxf(tmax, shfl_xor(tmax, 32));
+    const float m_new = fmaxf(m_run, tmax);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < C::NKB; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = exp2f(sacc[kb][i] - m_new);
+        sacc[kb][i] = p;
+        psum += p;
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int cb = 0; cb < C::CB; ++cb) oacc[cb] *= alpha;
+
+    // O^T += V^T P^T. P^T item i of sub-tile kb is key kb*32 + acc_row(lane, i); the
+    // 16-deep K step s2 takes items 8*s2..8*s2+7, so V^T slot e of lane half g2 is key
+    // kb*32 + 16*s2 + (e/4)*8 + 4*g2 + e%4.
+#pragma unroll
+    for (int kb = 0; kb < C::NKB; ++kb) {
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        Fr pf;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[e] = from_f32<T>(sacc[kb][s2 * 8 + e]);
+        const int kbase = kb * 32 + 16 * s2 + 4 * g2;
+#pragma unroll
+        for (int cb = 0; cb < C::CB; ++cb) {
+          const T* vcol = sv + cb * 32 + (lane & 31);
+          Fr vf;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) vf[e] = vcol[(kbase + (e >> 2) * 8 + (e & 3)) * C::PITCH];
+          mfma_k16(oacc[cb], vf, pf);
+        }
+      }
+    }
+  }
+
+  const float l_tot = l_run + shfl_xor(l_run, 32);
+  if (!row_ok) return;
+  const int64_t orow = ((int64_t)b * a.Nq + my_i) * a.Hq + my_h;
+  if (a.splits == 1) {
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    T* o = (T*)a.O + orow * HD;
+#pragma unroll
+    for (int cb = 0; cb < C::CB; ++cb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int c = cb * 32 + q4 * 8 + g2 * 4;
+        store4<T>(o + c, oacc[cb][q4 * 4] * inv, oacc[cb][q4 * 4 + 1] * inv,
+                  oacc[cb][q4 * 4 + 2] * inv, oacc[cb][q4 * 4 + 3] * inv);
+      }
+  } else {
+    const int64_t rows_total = (int64_t)a.B * a.Nq * a.Hq;
+    float* op = a.Opart + ((int64_t)split * rows_total + orow) * HD;
+#pragma unroll
+    for (int cb = 0; cb < C::CB; ++cb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int c = cb * 32 + q4 * 8 + g2 * 4;
+        *(f32x4*)(op + c) = f32x4{oacc[cb][q4 * 4], oacc[cb][q4 * 4 + 1], oacc[cb][q4 * 4 + 2],
+                                  oacc[cb][q4 * 4 + 3]};
+      }
+    if (g2 == 0) {
+      float* ml = a.MLpart + ((int64_t)split * rows_total + orow) * 2;
+      ml[0] = m_run;
+      ml[1] = l_tot;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ decode
+
+template <typename T, int HD, int MAXG>
+__global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
+  constexpr int NW = 4;
+  constexpr int LPK = HD / 8;      // lanes per key row (8 elements each)
+  constexpr int KPW = WAVE / LPK;  // keys per wave step
+  constexpr int U = 4;             // key steps in flight per lane
+  __shared__ float red_m[NW][MAXG], red_l[NW][MAXG];
+  __shared__ float red_o[NW][MAXG][HD];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane % LPK, grp = lane / LPK;
+  const int G = a.Hq / a.Hkv;
+  const int bg = blockIdx.x, b = bg / a.Hkv, g = bg - b * a.Hkv;
+  const int split = blockIdx.y;
+  const int nk = a.Nv + a.q_pos0 + 1;  // the single query sees every visual key and text 0..q_pos0
+  const int k_begin = split * a.keys_per_split;
+  const int k_end = min(nk, k_begin + a.keys_per_split);
+
+  const T* Kvb = (const T*)a.Kv + (int64_t)bg * a.Nv * HD + sub * 8;
+  const T* Vvb = (const T*)a.Vv + (int64_t)bg * a.Nv * HD + sub * 8;
+  const T* Ktb = (const T*)a.Kt + (int64_t)bg * a.Nkt * HD + sub * 8;
+  const T* Vtb = (const T*)a.Vt + (int64_t)bg * a.Nkt * HD + sub * 8;
+
+  float q[MAXG][8], o[MAXG][8], m[MAXG], l[MAXG];
+#pragma unroll
+  for (int h = 0; h < MAXG; ++h) {
+    m[h] = NEG_BIG;
+    l[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+    if (h < G) {
+      load_row8_f32<T>((const T*)a.Q + ((int64_t)b * a.Hq + g * G + h) * HD + sub * 8, q[h]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q[h][e] *= a.scale_log2;
+    }
+  }
+
+  const int stride = NW * KPW;
+  for (int j0 = k_begin + wave * KPW + grp; j0 < k_end; j0 += stride * U) {
+    float kx[U][8], vx[U][8];
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * stride;
+      ok[u] = j < k_end;
+      if (ok[u]) {
+        load_row8_f32<T>(j < a.Nv ? Kvb + (int64_t)j * HD : Ktb + (int64_t)(j - a.Nv) * HD, kx[u]);
+        load_row8_f32<T>(j < a.Nv ? Vvb + (int64_t)j * HD : Vtb + (int64_t)(j - a.Nv) * HD, vx[u]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kx[u][e] = vx[u][e] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < MAXG; ++h) {
+      if (h >= G) break;
+      float s[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(q[h][e], kx[u][e], acc);
+#pragma unroll
+        for (int w = 1; w < LPK; w <<= 1) acc += shfl_xor(acc, w);
+        s[u] = ok[u] ? acc : -INFINITY;
+      }
+      float mx = m[h];
+#pragma unroll
+      for (int u = 0; u < U; ++u) mx = fmaxf(mx, s[u]);
+      const float alpha = exp2f(m[h] - mx);
+      m[h] = mx;
+      float ps = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] *= alpha;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float p = exp2f(s[u] - mx);
+        ps += p;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(p, vx[u][e], o[h][e]);
+      }
+      l[h] = l[h] * alpha + ps;
+    }
+  }
+
+  // Merge the key groups of the wave (lanes differing in the bits above LPK).
+#pragma unroll
+  for (int w = LPK; w < WAVE; w <<= 1) {
+#pragma unroll
+    for (int h = 0; h < MAXG; ++h) {
+      if (h >= G) break;
+      const float mo = shfl_xor(m[h], w), lo = shfl_xor(l[h], w);
+      const float mx = fmaxf(m[h], mo);
+      const float sa = exp2f(m[h] - mx), sb = exp2f(mo - mx);
+      l[h] = l[h] * sa + lo * sb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] = o[h][e] * sa + shfl_xor(o[h][e], w) * sb;
+      m[h] = mx;
+    }
+  }
+  if (grp == 0) {
+#pragma unroll
+    for (int h = 0; h < MAXG; ++h) {
+      if (h >= G) break;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red_o[wave][h][sub * 8 + e] = o[h][e];
+      if (sub == 0) {
+        red_m[wave][h] = m[h];
+        red_l[wave][h] = l[h];
+      }
+    }
+  }
+  __syncthreads();
+  // Merge the waves: thread t handles (head h, channel c).
+  for (int t = tid; t < G * HD; t += NW * WAVE) {
+    const int h = t / HD, c = t - h * HD;
+    float mx = NEG_BIG;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) mx = fmaxf(mx, red_m[w][h]);
+    float lt = 0.f, ot = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float sc = exp2f(red_m[w][h] - mx);
+      lt += red_l[w][h] * sc;
+      ot += red_o[w][h][c] * sc;
+    }
+    const int64_t orow = (int64_t)b * a.Hq + g * G + h;
+    if (a.splits == 1) {
+      ((T*)a.O)[orow * HD + c] = from_f32<T>(lt > 0.f ? ot / lt : 0.f);
+    } else {
+      const int64_t rows_total = (int64_t)a.B * a.Hq;
+      a.Opart[((int64_t)split * rows_total + orow) * HD + c] = ot;
+      if (c == 0) {
+        float* ml = a.MLpart + ((int64_t)split * rows_total + orow) * 2;
+        ml[0] = mx;
+        ml[1] = lt;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ combine
+
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ Opart,
+                                                      const float* __restrict__ MLpart,
+                                                      T* __restrict__ O, int64_t rows, int splits) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  constexpr int CPR = HD / 4;
+  if (t >= rows * CPR) return;
+  const int64_t row = t / CPR;
+  const int c = (int)(t - row * CPR) * 4;
+  float mx = NEG_BIG;
+  for (int s = 0; s < splits; ++s) mx = fmaxf(mx, MLpart[((int64_t)s * rows + row) * 2]);
+  float lt = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < splits; ++s) {
+    const float* ml = MLpart + ((int64_t)s * rows + row) * 2;
+    const float sc = exp2f(ml[0] - mx);
+    lt += ml[1] * sc;
+    acc += *(const f32x4*)(Opart + ((int64_t)s * rows + row) * HD + c) * sc;
+  }
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+  store4<T>(O + row * HD + c, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+}
+
+// ------------------------------------------------------------------ host side
+
+static inline int64_t cdiv64(int64_t x, int64_t y) { return (x + y - 1) / y; }
+
+AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt, int q_pos0,
+                        size_t ws_bytes) {
+  AttnPlan p{};
+  const int G = Hq / Hkv;
+  const int64_t rows_total = (int64_t)B * Nq * Hq;
+  const int64_t per_split = rows_total * (int64_t)(hd + 2) * 4;
+  const int max_keys = Nv + q_pos0 + Nq;  // keys seen by the last query
+  p.decode = (Nq == 1 && G <= 8);
+  int units, key_gran;
+  if (p.decode) {
+    p.nw = 4;
+    units = B * Hkv;
+    key_gran = 64;
+  } else {
+    const int R = Nq * G;
+    p.nw = R <= 32 ? 1 : (R <= 64 ? 2 : 4);
+    p.row_blocks = (int)cdiv64(R, 32 * p.nw);
+    units = B * Hkv * p.row_blocks;
+    key_gran = 64;
+  }
+  // Enough blocks to fill 256 CUs twice, keeping at least two key tiles per split.
+  const int64_t tiles = cdiv64(max_keys, key_gran);
+  int64_t want = cdiv64(512, units);
+  want = std::min<int64_t>(want, std::max<int64_t>(1, tiles / 2));
+  want = std::max<int64_t>(1, std::min<int64_t>(want, 64));
+  if (want > 1 && per_split > 0) {
+    const int64_t fit = (int64_t)(ws_bytes / (size_t)per_split);
+    want = std::min<int64_t>(want, fit);
+    if (want < 2) want = 1;
+  }
+  p.splits = (int)want;
+  const int64_t tiles_per_split = cdiv64(tiles, p.splits);
+  p.keys_per_split = (int)(tiles_per_split * key_gran);
+  p.splits = (int)cdiv64(tiles, tiles_per_split);  // drop empty trailing splits
+  p.ws_needed = p.splits > 1 ? (size_t)(p.splits * per_split) : 0;
+  return p;
+}
+
+size_t attention_workspace(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt) {
+  AttnPlan p = plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, Nkt - Nq, (size_t)-1);
+  return p.ws_needed;
+}
+
+template <typename T, int HD>
+static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_t s,
+                                const LaunchEvents& ev) {
+  record(ev.attn[0], s);
+  if (p.decode) {
+    dim3 grid(a.B * a.Hkv, p.splits);
+    const int G = a.Hq / a.Hkv;
+    if (G == 1)
+      k_attn_decode<T, HD, 1><<<grid, dim3(256), 0, s>>>(a);
+    else if (G == 2)
+      k_attn_decode<T, HD, 2><<<grid, dim3(256), 0, s>>>(a);
+    else if (G <= 4)
+      k_attn_decode<T, HD, 4><<<grid, dim3(256), 0, s>>>(a);
+    else
+      k_attn_decode<T, HD, 8><<<grid, dim3(256), 0, s>>>(a);
+  } else {
+    dim3 grid(p.row_blocks, a.B * a.Hkv, p.splits);
+    if (p.nw == 1)
+      k_attn_prefill<T, HD, 1><<<grid, dim3(64), AttnCfg<T, HD, 1>::LDS_BYTES, s>>>(a);
+    else if (p.nw == 2)
+      k_attn_prefill<T, HD, 2><<<grid, dim3(128), AttnCfg<T, HD, 2>::LDS_BYTES, s>>>(a);
+    else
+      k_attn_prefill<T, HD, 4><<<grid, dim3(256), AttnCfg<T, HD, 4>::LDS_BYTES, s>>>(a);
+  }
+  record(ev.attn[1], s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.splits == 1) return e;
+  const int64_t rows = (int64_t)a.B * a.Nq * a.Hq;
+  const int64_t threads = rows * (HD / 4);
+  k_attn_combine<T, HD><<<dim3((unsigned)cdiv64(threads, 256)), dim3(256), 0, s>>>((const float*)a.Opart, (const float*)a.MLpart, (T*)a.O, rows, p.splits);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int dtype, hipStream_t s,
+                            const LaunchEvents& ev) {
+  if (dtype == 1) {
+    if (a.hd == 128) return attn_launch_t<bf16, 128>(a, p, s, ev);
+    return attn_launch_t<bf16, 64>(a, p, s, ev);
+  }
+  if (a.hd == 128) return attn_launch_t<float, 128>(a, p, s, ev);
+  return attn_launch_t<float, 64>(a, p, s, ev);
+}
+
+}  // namespace dv

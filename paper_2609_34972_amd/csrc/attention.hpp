@@ -1,0 +1,43 @@
+// Host-side interface of the text-query attention kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "build_kernels.hpp"
+
+namespace dv {
+
+struct AttnArgs {
+  const void* Q;
+  const void* Kv;
+  const void* Vv;
+  const void* Kt;
+  const void* Vt;
+  void* O;
+  float* Opart;   // [splits, B*Nq*Hq, hd] unnormalised partial outputs (splits > 1)
+  float* MLpart;  // [splits, B*Nq*Hq, 2]  running max (log2 domain) and sum
+  int B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0;
+  float scale_log2;  // softmax scale times log2(e)
+  int splits, keys_per_split;
+};
+
+struct AttnPlan {
+  bool decode;         // one query per sequence: the bandwidth-bound kernel
+  int nw;              // waves per block (prefill)
+  int row_blocks;      // blocks along the packed (query, head) rows (prefill)
+  int splits;          // key splits merged by a log-sum-exp combine
+  int keys_per_split;  // multiple of the 64-key tile
+  size_t ws_needed;    // bytes of partials for this plan
+};
+
+AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt, int q_pos0,
+                        size_t ws_bytes);
+size_t attention_workspace(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt);
+hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int dtype, hipStream_t s,
+                            const LaunchEvents& ev);
+
+}  // namespace dv

@@ -1,0 +1,277 @@
+// Visual-memory build and visual K/V projection on gfx950.
+//
+//   k_down_act   Section 3.1 Eq. 4-5, down half, all layers in one GEMM:
+//                Z[l] = phi(E D_l), phi applied to the fp32 accumulators.
+//   k_up_norm    Eq. 4-5 up half + residual: M_l = E + Z_l U_l. Writes the
+//                memory already multiplied by the RMSNorm weight, rounded to
+//                the call dtype, plus fp32 partial sums of M_l^2 per row and
+//                column tile (the norm needs the whole row; the partials let
+//                the projection finish it without a second pass over M_l).
+//   k_kv_proj    Section 3.2 Eq. 7: [Kv | Vv] = (M_l * gamma_l) [Wk | Wv]^T,
+//                scaled per row by rsqrt(mean(M_l^2) + eps) in the epilogue
+//                (the RMSNorm factor is a per-row scalar, so it commutes with
+//                the product), stored head-major [B, Hkv, Nv, hd].
+#include "build_kernels.hpp"
+#include "gemm_tile.hpp"
+
+namespace dv {
+
+// ---------------------------------------------------------------- tiles
+
+template <typename T> struct BuildTiles;
+template <> struct BuildTiles<bf16> {
+  typedef TileCfg<bf16, 128, 128, 2, 2> Down;
+  typedef TileCfg<bf16, 128, 128, 2, 2> Up;
+  typedef TileCfg<bf16, 128, 128, 2, 2> KV;
+};
+template <> struct BuildTiles<float> {
+  typedef TileCfg<float, 64, 64, 2, 2> Down;
+  typedef TileCfg<float, 64, 64, 2, 2> Up;
+  typedef TileCfg<float, 64, 64, 2, 2> KV;
+};
+
+// ---------------------------------------------------------------- K-a
+
+template <class C, int ACT>
+__global__ __launch_bounds__(C::NT) void k_down_act(const typename C::elem* __restrict__ E,
+                                                    const typename C::elem* __restrict__ Dw,
+                                                    typename C::elem* __restrict__ Z, int T,
+                                                    int d, int L, int r) {
+  typedef typename C::elem Tp;
+  extern __shared__ __align__(16) unsigned char smem[];
+  Tp* lds = (Tp*)smem;
+  const int N = L * r;
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  f32x16 acc[C::FM][C::FN];
+  BRows<Tp> B{Dw, Dw, (int64_t)d, N};
+  gemm_nt_mainloop<C>(E, d, T, B, N, d, m0, n0, lds, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+#pragma unroll
+  for (int b = 0; b < C::FN; ++b) {
+    const int col = n0 + wn * C::WN + b * 32 + (lane & 31);
+    if (col >= N) continue;
+    const int l = col / r, j = col - l * r;
+    Tp* zl = Z + (int64_t)l * T * r + j;
+#pragma unroll
+    for (int a = 0; a < C::FM; ++a) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int row = m0 + wm * C::WM + a * 32 + acc_row(lane, i);
+        if (row < T) {
+          const float x = acc[a][b][i];
+          zl[(int64_t)row * r] = from_f32<Tp>(ACT == 0 ? silu(x) : gelu(x));
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- up + residual
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void k_up_norm(const typename C::elem* __restrict__ E,
+                                                   const typename C::elem* __restrict__ Z,
+                                                   const typename C::elem* __restrict__ Uw,
+                                                   const typename C::elem* __restrict__ gamma,
+                                                   typename C::elem* __restrict__ Mg,
+                                                   float* __restrict__ ssq, int T, int d, int r,
+                                                   int l0) {
+  typedef typename C::elem Tp;
+  extern __shared__ __align__(16) unsigned char smem[];
+  Tp* lds = (Tp*)smem;
+  const int lz = blockIdx.z, l = l0 + lz;
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const Tp* Zl = Z + (int64_t)l * T * r;
+  const Tp* Ul = Uw + (int64_t)l * d * r;
+  f32x16 acc[C::FM][C::FN];
+  BRows<Tp> B{Ul, Ul, (int64_t)r, d};
+  gemm_nt_mainloop<C>(Zl, r, T, B, d, r, m0, n0, lds, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const Tp* gl = gamma + (int64_t)l * d;
+  Tp* Ml = Mg + (int64_t)lz * T * d;
+  float part[C::FM][16];
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) part[a][i] = 0.f;
+
+#pragma unroll
+  for (int b = 0; b < C::FN; ++b) {
+    const int col = n0 + wn * C::WN + b * 32 + (lane & 31);
+    if (col >= d) continue;
+    const float g = to_f32(gl[col]);
+#pragma unroll
+    for (int a = 0; a < C::FM; ++a) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int row = m0 + wm * C::WM + a * 32 + acc_row(lane, i);
+        if (row < T) {
+          const float m = acc[a][b][i] + to_f32(E[(int64_t)row * d + col]);
+          part[a][i] += m * m;
+          Ml[(int64_t)row * d + col] = from_f32<Tp>(m * g);
+        }
+      }
+    }
+  }
+  // Sum the squares over the 32 columns held by each half-wave, then over the
+  // WGN waves sharing the rows; one partial per (row, column tile).
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float v = part[a][i];
+      v += shfl_xor(v, 1);
+      v += shfl_xor(v, 2);
+      v += shfl_xor(v, 4);
+      v += shfl_xor(v, 8);
+      v += shfl_xor(v, 16);
+      part[a][i] = v;
+    }
+  float* red = (float*)smem;  // [WGN][BM]; the main loop ended with a barrier
+  if ((lane & 31) == 0) {
+#pragma unroll
+    for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) red[wn * C::BM + wm * C::WM + a * 32 + acc_row(lane, i)] = part[a][i];
+  }
+  __syncthreads();
+  const int np = (d + C::BN - 1) / C::BN;
+  for (int rr = threadIdx.x; rr < C::BM; rr += C::NT) {
+    const int row = m0 + rr;
+    if (row < T) {
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < C::WGN; ++w) s += red[w * C::BM + rr];
+      ssq[((int64_t)lz * np + blockIdx.x) * T + row] = s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- K/V projection
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void k_kv_proj(const typename C::elem* __restrict__ Mg,
+                                                   const float* __restrict__ ssq,
+                                                   const typename C::elem* __restrict__ Wk,
+                                                   const typename C::elem* __restrict__ Wv,
+                                                   typename C::elem* __restrict__ Kv,
+                                                   typename C::elem* __restrict__ Vv, int B_,
+                                                   int Nv, int d, int Hkv, int hd, int l0,
+                                                   int np, float eps) {
+  typedef typename C::elem Tp;
+  extern __shared__ __align__(16) unsigned char smem[];
+  Tp* lds = (Tp*)smem;
+  const int T = B_ * Nv, kv = Hkv * hd, N = 2 * kv;
+  const int lz = blockIdx.z, l = l0 + lz;
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const Tp* Ml = Mg + (int64_t)lz * T * d;
+  f32x16 acc[C::FM][C::FN];
+  BRows<Tp> Bw{Wk + (int64_t)l * kv * d, Wv + (int64_t)l * kv * d, (int64_t)d, kv};
+  gemm_nt_mainloop<C>(Ml, d, T, Bw, N, d, m0, n0, lds, acc);
+
+  // Row scale of the RMSNorm from the partial sums of squares.
+  float* rs = (float*)smem;  // [BM]
+  for (int rr = threadIdx.x; rr < C::BM; rr += C::NT) {
+    const int row = m0 + rr;
+    float s = 0.f;
+    if (row < T)
+      for (int p = 0; p < np; ++p) s += ssq[((int64_t)lz * np + p) * T + row];
+    rs[rr] = rsqrtf(s / (float)d + eps);
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int64_t head_stride = (int64_t)Nv * hd;
+  const int64_t layer_stride = (int64_t)B_ * Hkv * head_stride;
+#pragma unroll
+  for (int b = 0; b < C::FN; ++b) {
+    const int col = n0 + wn * C::WN + b * 32 + (lane & 31);
+    if (col >= N) continue;
+    Tp* out = col < kv ? Kv : Vv;
+    const int o = col < kv ? col : col - kv;
+    const int h = o / hd, c = o - h * hd;
+    Tp* base = out + (int64_t)l * layer_stride + (int64_t)h * head_stride + c;
+#pragma unroll
+    for (int a = 0; a < C::FM; ++a) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int rl = wm * C::WM + a * 32 + acc_row(lane, i);
+        const int row = m0 + rl;
+        if (row < T) {
+          const int bb = row / Nv, ii = row - bb * Nv;
+          base[(int64_t)bb * Hkv * head_stride + (int64_t)ii * hd] = from_f32<Tp>(acc[a][b][i] * rs[rl]);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+
+static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+template <typename T>
+static hipError_t down_launch(const void* E, const void* Dw, void* Z, int T_, int d, int L, int r,
+                              int act, hipStream_t s, const LaunchEvents& ev) {
+  typedef typename BuildTiles<T>::Down C;
+  dim3 grid(cdiv((int64_t)L * r, C::BN), cdiv(T_, C::BM));
+  record(ev.down[0], s);
+  if (act == 0)
+    k_down_act<C, 0><<<grid, dim3(C::NT), C::LDS_BYTES, s>>>((const T*)E, (const T*)Dw, (T*)Z, T_, d, L, r);
+  else
+    k_down_act<C, 1><<<grid, dim3(C::NT), C::LDS_BYTES, s>>>((const T*)E, (const T*)Dw, (T*)Z, T_, d, L, r);
+  record(ev.down[1], s);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, int d, int L,
+                           int r, int act, int dtype, hipStream_t s, const LaunchEvents& ev) {
+  if (dtype == 1) return down_launch<bf16>(E, Dw, Z, (int)T_, d, L, r, act, s, ev);
+  return down_launch<float>(E, Dw, Z, (int)T_, d, L, r, act, s, ev);
+}
+
+int kv_partials(int d, int dtype) {
+  return dtype == 1 ? cdiv(d, BuildTiles<bf16>::Up::BN) : cdiv(d, BuildTiles<float>::Up::BN);
+}
+
+template <typename T>
+static hipError_t kv_launch(const void* E, const void* Z, const void* Uw, const void* gamma,
+                            const void* Wk, const void* Wv, void* Kv, void* Vv, int B_, int Nv,
+                            int d, int r, int Hkv, int hd, int l0, int nl, float eps, void* Mg,
+                            float* ssq, hipStream_t s, const LaunchEvents& ev, bool first,
+                            bool last) {
+  typedef typename BuildTiles<T>::Up CU;
+  typedef typename BuildTiles<T>::KV CK;
+  const int T_ = B_ * Nv;
+  const int np = cdiv(d, CU::BN);
+  dim3 gu(np, cdiv(T_, CU::BM), nl);
+  if (first) record(ev.up[0], s);
+  k_up_norm<CU><<<gu, dim3(CU::NT), CU::LDS_BYTES, s>>>((const T*)E, (const T*)Z, (const T*)Uw, (const T*)gamma, (T*)Mg, ssq, T_, d, r, l0);
+  if (last) record(ev.up[1], s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 gk(cdiv(2 * Hkv * hd, CK::BN), cdiv(T_, CK::BM), nl);
+  if (first) record(ev.kv[0], s);
+  k_kv_proj<CK><<<gk, dim3(CK::NT), CK::LDS_BYTES, s>>>((const T*)Mg, ssq, (const T*)Wk, (const T*)Wv, (T*)Kv, (T*)Vv, B_, Nv, d, Hkv, hd, l0, np, eps);
+  if (last) record(ev.kv[1], s);
+  return hipGetLastError();
+}
+
+hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
+                             const void* Wk, const void* Wv, void* Kv, void* Vv, int B_, int Nv,
+                             int d, int r, int Hkv, int hd, int l0, int nl, float eps, int dtype,
+                             void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
+                             bool first, bool last) {
+  if (dtype == 1)
+    return kv_launch<bf16>(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv, hd, l0, nl, eps,
+                           Mg, ssq, s, ev, first, last);
+  return kv_launch<float>(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv, hd, l0, nl, eps,
+                          Mg, ssq, s, ev, first, last);
+}
+
+}  // namespace dv

@@ -1,0 +1,36 @@
+// Host-side launchers of the visual-memory build kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dv {
+
+// Optional hipEvent pairs recorded around kernel launches (profiling hook).
+struct LaunchEvents {
+  hipEvent_t down[2] = {nullptr, nullptr};
+  hipEvent_t up[2] = {nullptr, nullptr};
+  hipEvent_t kv[2] = {nullptr, nullptr};
+  hipEvent_t attn[2] = {nullptr, nullptr};
+};
+
+inline void record(hipEvent_t e, hipStream_t s) {
+  if (e) (void)hipEventRecord(e, s);
+}
+
+// Z[l] = phi(E D_l) for all layers (dtype 0 = fp32, 1 = bf16; act 0 = SiLU, 1 = GELU).
+hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T, int d, int L, int r,
+                           int act, int dtype, hipStream_t s, const LaunchEvents& ev);
+
+// Number of fp32 partial sums of squares per row written by the up kernel.
+int kv_partials(int d, int dtype);
+
+// Layers l0..l0+nl-1: memory, RMSNorm and K/V projection. Mg holds nl*T*d
+// elements of the call dtype and ssq nl*kv_partials(d)*T floats.
+hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
+                             const void* Wk, const void* Wv, void* Kv, void* Vv, int B, int Nv,
+                             int d, int r, int Hkv, int hd, int l0, int nl, float eps, int dtype,
+                             void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
+                             bool first_group, bool last_group);
+
+}  // namespace dv

@@ -1,0 +1,136 @@
+"""C-ABI boundary checks that need no GPU.
+
+The library must load, export every function that include/deltavision.h
+declares, and reject invalid arguments on the host (before any HIP call) with
+the documented status codes. Only NULL or fake pointers are passed: every case
+here fails validation, so nothing is ever launched.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_34972_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "deltavision.h")
+
+OK, NULL, SHAPE, UNSUP, ALIGN, WS = 0, 1, 2, 3, 4, 5
+F32, BF16 = 0, 1
+FAKE = 0x10000  # a 16-byte aligned non-NULL address; never dereferenced (validation fails first)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dv_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2609_34972_amd import build
+        build.build()
+    return _lib.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(_lib.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+        assert ctypes.cast(getattr(lib, n), ctypes.c_void_p).value
+
+
+def test_version_and_status_strings(lib):
+    assert lib.dv_abi_version() == 1
+    for code, name in [(0, b"DV_OK"), (1, b"DV_ERR_NULL"), (2, b"DV_ERR_SHAPE"),
+                       (3, b"DV_ERR_UNSUPPORTED"), (4, b"DV_ERR_ALIGN"), (5, b"DV_ERR_WORKSPACE"),
+                       (6, b"DV_ERR_HIP"), (7, b"DV_ERR_INTERNAL"), (99, b"DV_UNKNOWN_STATUS")]:
+        assert lib.dv_status_string(code) == name
+
+
+def build_call(lib, E=FAKE, Dw=FAKE, Z=FAKE, T=64, d=256, L=4, r=16, act=0, dt=F32):
+    return lib.dv_build_visual_memory(E, Dw, Z, T, d, L, r, act, dt, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(E=None), NULL), (dict(Dw=None), NULL), (dict(Z=None), NULL),
+    (dict(E=FAKE + 4), ALIGN), (dict(Z=FAKE + 8), ALIGN),
+    (dict(T=0), SHAPE), (dict(T=-5), SHAPE), (dict(d=0), SHAPE), (dict(L=0), SHAPE), (dict(r=0), SHAPE),
+    (dict(T=65535 * 64 + 1), SHAPE),
+    (dict(d=100), UNSUP), (dict(r=24), UNSUP), (dict(act=7), UNSUP), (dict(dt=5), UNSUP),
+])
+def test_build_visual_memory_rejects(lib, kw, code):
+    assert build_call(lib, **kw) == code
+    assert lib.dv_last_error() != b""
+
+
+def kv_call(lib, ws=FAKE, ws_bytes=None, **over):
+    a = dict(E=FAKE, Z=FAKE, Uw=FAKE, g=FAKE, Wk=FAKE, Wv=FAKE, Kv=FAKE, Vv=FAKE, B=1, Nv=64, d=256,
+             L=4, r=16, Hkv=4, hd=64, l0=0, nl=4, eps=1e-5, dt=F32)
+    a.update(over)
+    if ws_bytes is None:
+        ws_bytes = lib.dv_project_visual_kv_workspace(a["B"] * a["Nv"], a["d"], a["nl"], a["dt"])
+    return lib.dv_project_visual_kv(a["E"], a["Z"], a["Uw"], a["g"], a["Wk"], a["Wv"], a["Kv"],
+                                    a["Vv"], a["B"], a["Nv"], a["d"], a["L"], a["r"], a["Hkv"],
+                                    a["hd"], a["l0"], a["nl"], a["eps"], a["dt"], ws, ws_bytes,
+                                    None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(E=None), NULL), (dict(Wv=None), NULL), (dict(Kv=None), NULL), (dict(g=None), NULL),
+    (dict(Wk=FAKE + 2), ALIGN),
+    (dict(B=0), SHAPE), (dict(Nv=0), SHAPE), (dict(l0=-1), SHAPE), (dict(nl=0), SHAPE),
+    (dict(l0=2, nl=3), SHAPE), (dict(eps=-1.0), SHAPE), (dict(eps=float("nan")), SHAPE),
+    (dict(hd=96), UNSUP), (dict(d=96), UNSUP), (dict(r=8), UNSUP), (dict(dt=2), UNSUP),
+])
+def test_project_visual_kv_rejects(lib, kw, code):
+    assert kv_call(lib, **kw) == code
+
+
+def test_project_visual_kv_workspace_rules(lib):
+    one = lib.dv_project_visual_kv_workspace(64, 256, 1, F32)
+    four = lib.dv_project_visual_kv_workspace(64, 256, 4, F32)
+    assert one > 64 * 256 * 4 and four == 4 * one
+    assert lib.dv_project_visual_kv_workspace(64, 256, 1, BF16) < one
+    assert lib.dv_project_visual_kv_workspace(0, 256, 1, F32) == 0
+    assert lib.dv_project_visual_kv_workspace(64, 256, 1, 9) == 0
+    assert kv_call(lib, ws=None) == WS
+    assert kv_call(lib, ws_bytes=one - 1) == WS
+    assert kv_call(lib, ws=FAKE + 4, ws_bytes=one) == ALIGN
+
+
+def attn_call(lib, ws=None, ws_bytes=0, **over):
+    a = dict(Q=FAKE, Kv=FAKE, Vv=FAKE, Kt=FAKE, Vt=FAKE, O=FAKE, B=1, Hq=4, Hkv=4, hd=64, Nv=64,
+             Nq=16, Nkt=16, q0=0, scale=0.125, dt=F32)
+    a.update(over)
+    return lib.dv_text_visual_attention(a["Q"], a["Kv"], a["Vv"], a["Kt"], a["Vt"], a["O"], a["B"],
+                                        a["Hq"], a["Hkv"], a["hd"], a["Nv"], a["Nq"], a["Nkt"],
+                                        a["q0"], a["scale"], a["dt"], ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Q=None), NULL), (dict(Kt=None), NULL), (dict(O=None), NULL), (dict(Kv=None), NULL),
+    (dict(Vt=FAKE + 4), ALIGN),
+    (dict(B=0), SHAPE), (dict(Nq=0), SHAPE), (dict(Nv=-1), SHAPE), (dict(q0=-1), SHAPE),
+    (dict(Hq=6, Hkv=4), SHAPE), (dict(q0=1), SHAPE), (dict(Nkt=15), SHAPE),
+    (dict(scale=float("inf")), SHAPE), (dict(B=70000, Hkv=1, Hq=1), SHAPE),
+    (dict(hd=32), UNSUP), (dict(hd=256), UNSUP), (dict(dt=3), UNSUP),
+])
+def test_text_visual_attention_rejects(lib, kw, code):
+    assert attn_call(lib, **kw) == code
+
+
+def test_attention_misaligned_workspace_rejected(lib):
+    assert attn_call(lib, ws=FAKE + 4, ws_bytes=1 << 20) == ALIGN
+
+
+def test_attention_workspace_query(lib):
+    # Few (batch, head) units with many keys want a key split, hence a workspace.
+    n = lib.dv_text_visual_attention_workspace(1, 28, 4, 128, 16384, 128, 128)
+    assert n > 0 and n % (1 * 128 * 28 * (128 + 2) * 4) == 0
+    # Decode over 2048 (batch, head) streams fills the chip without a split.
+    assert lib.dv_text_visual_attention_workspace(64, 32, 32, 128, 576, 1, 513) == 0
+    assert lib.dv_text_visual_attention_workspace(1, 6, 4, 128, 10, 4, 4) == 0  # invalid GQA

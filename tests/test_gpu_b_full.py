@@ -1,0 +1,93 @@
+"""GPU parity at the full workload sizes, in the launch configuration the benchmark times.
+
+The whole batch runs on the GPU exactly as in the benchmark (all layers in one
+call, the recommended workspace); the oracle then recomputes seeded samples of
+the outputs one row or one (batch, kv-head) group at a time. Every output row
+depends only on its own token (build) or its own group (attention), so the
+sampled rows are complete checks of those outputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_34972_amd as dvl
+from paper_2609_34972_amd import configs, synth
+from tests.gpu_helpers import assert_close, cuda, f64, say
+
+pytestmark = pytest.mark.gpu
+
+BUILD_FULL = [configs.LLAVA7B, configs.QWEN25VL_VIDEO, configs.LLAVA_NEXT]
+ATTN_FULL = [configs.LLAVA7B, configs.QWEN25VL_VIDEO, configs.LLAVA_NEXT, configs.DECODE]
+
+
+@pytest.mark.parametrize("w", BUILD_FULL, ids=lambda w: w.name)
+def test_full_build_sampled(w):
+    say(f"[full build {w.name}] generating inputs")
+    E = synth.make_E(w)
+    wts = synth.make_build_weights(w)
+    Eg = cuda(E)
+    wg = {k: cuda(v) for k, v in wts.items()}
+    dt = Eg.dtype
+    say(f"[full build {w.name}] running on GPU")
+    Z = torch.empty(w.L, w.T, w.r, dtype=dt, device="cuda:0")
+    dvl.build_visual_memory(Eg, wg["Dw"], Z, act=w.act)
+    Kv = torch.empty(w.L, w.B, w.Hkv, w.Nv, w.hd, dtype=dt, device="cuda:0")
+    Vv = torch.empty_like(Kv)
+    ws = torch.empty(dvl.project_visual_kv_workspace(w.T, w.d, w.L, dt), dtype=torch.uint8,
+                     device="cuda:0")
+    dvl.project_visual_kv(Eg, Z, wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv, Vv, eps=w.eps, ws=ws)
+    torch.cuda.synchronize()
+    del ws, wg
+    rng = np.random.default_rng(1234)
+    # Z: 256 sampled tokens, every layer.
+    rows = np.sort(rng.choice(w.T, 256, replace=False))
+    E64 = f64(E[torch.from_numpy(rows)])
+    Zr = oracle.down(E64, f64(wts["Dw"]), w.act)
+    Zg = f64(Z[:, torch.from_numpy(rows)])
+    for l in range(w.L):
+        assert_close(Zg[l], Zr[l], w.dtype, f"Z layer {l}")
+    # Kv / Vv: 64 sampled tokens, layers 0, L-1 and two random ones.
+    layers = sorted({0, w.L - 1, *rng.choice(np.arange(1, w.L - 1), 2, replace=False).tolist()})
+    rows = np.sort(rng.choice(w.T, 64, replace=False))
+    E64 = f64(E[torch.from_numpy(rows)])
+    li = torch.tensor(layers)
+    say(f"[full build {w.name}] oracle on {len(rows)} rows x layers {layers}")
+    Zl = oracle.down(E64, f64(wts["Dw"][li]), w.act)
+    Kr, Vr = oracle.project_visual_kv(E64, Zl, f64(wts["Uw"][li]), f64(wts["gamma"][li]),
+                                      f64(wts["Wk"][li]), f64(wts["Wv"][li]), 1, len(rows), w.Hkv,
+                                      w.hd, w.eps)
+    b_idx = torch.from_numpy(rows // w.Nv)
+    i_idx = torch.from_numpy(rows % w.Nv)
+    for n, l in enumerate(layers):
+        kg = f64(Kv[l][b_idx, :, i_idx, :])   # [rows, Hkv, hd]
+        vg = f64(Vv[l][b_idx, :, i_idx, :])
+        ek = assert_close(kg, Kr[n, 0].transpose(1, 0, 2), w.dtype, f"Kv layer {l}")
+        ev = assert_close(vg, Vr[n, 0].transpose(1, 0, 2), w.dtype, f"Vv layer {l}")
+        say(f"  layer {l}: Kv {ek:.2e} Vv {ev:.2e}")
+
+
+@pytest.mark.parametrize("w", ATTN_FULL, ids=lambda w: w.name)
+def test_full_attention_sampled(w):
+    say(f"[full attention {w.name}] generating inputs")
+    tx = synth.make_text(w, layers=[0])
+    vc = synth.make_visual_cache(w, layers=[0])
+    x = {k: v[0] for k, v in {**tx, **vc}.items()}
+    xg = {k: cuda(v) for k, v in x.items()}
+    O = torch.empty_like(xg["Q"])
+    n = dvl.text_visual_attention_workspace(w.B, w.Hq, w.Hkv, w.hd, w.Nv, w.Nq, w.Nkt)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device="cuda:0")
+    say(f"[full attention {w.name}] running on GPU")
+    dvl.text_visual_attention(xg["Q"], xg["Kv"], xg["Vv"], xg["Kt"], xg["Vt"], O, q_pos0=w.q_pos0,
+                              ws=ws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(99)
+    G = w.G
+    groups = [(int(b), int(g)) for b, g in zip(rng.integers(0, w.B, 4), rng.integers(0, w.Hkv, 4))]
+    for b, g in groups:
+        hs = slice(g * G, (g + 1) * G)
+        ref = oracle.text_visual_attention(
+            f64(x["Q"][b:b + 1, :, hs]), f64(x["Kv"][b:b + 1, g:g + 1]), f64(x["Vv"][b:b + 1, g:g + 1]),
+            f64(x["Kt"][b:b + 1, g:g + 1]), f64(x["Vt"][b:b + 1, g:g + 1]), w.q_pos0)
+        e = assert_close(f64(O[b:b + 1, :, hs]), ref, w.dtype, f"O batch {b} kv-head {g}")
+        say(f"  (b={b}, g={g}): {e:.2e}")
