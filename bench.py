@@ -31,6 +31,42 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+class HipEvents:
+    """Raw hipEvent_t handles from the HIP runtime (the library records them itself)."""
+
+    def __init__(self):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.made = []
+
+    def new(self) -> int:
+        h = self.ct.c_void_p()
+        if self.hip.hipEventCreate(self.ct.byref(h)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        self.made.append(h.value)
+        return h.value
+
+    def pair(self):
+        return self.new(), self.new()
+
+    def ms(self, pair) -> float:
+        out = self.ct.c_float()
+        rc = self.hip.hipEventElapsedTime(self.ct.byref(out), pair[0], pair[1])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(out.value)
+
+    def close(self):
+        for h in self.made:
+            self.hip.hipEventDestroy(h)
+        self.made = []
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -128,9 +164,10 @@ def run_prefill(args, w):
         step()
     torch.cuda.synchronize()
 
+    hev = HipEvents()
+    evs = [{"down": hev.pair(), "up": hev.pair(), "kv": hev.pair(),
+            "attn": [hev.pair() for _ in range(w.L)]} for _ in range(args.steps)]
     mk = lambda: torch.cuda.Event(enable_timing=True)
-    evs = [{"down": (mk(), mk()), "up": (mk(), mk()), "kv": (mk(), mk()),
-            "attn": [(mk(), mk()) for _ in range(w.L)]} for _ in range(args.steps)]
     t_begin, t_end = mk(), mk()
     log(f"[bench] timing {args.steps} steps")
     torch.cuda.synchronize()
@@ -143,9 +180,10 @@ def run_prefill(args, w):
         dvl.time_kernel(k)
     ms_total = t_begin.elapsed_time(t_end)
     ms_step = ms_total / args.steps
-    avg = lambda key: sum(e[key][0].elapsed_time(e[key][1]) for e in evs) / args.steps
+    avg = lambda key: sum(hev.ms(e[key]) for e in evs) / args.steps
     ms_down, ms_up, ms_kv = avg("down"), avg("up"), avg("kv")
-    ms_attn_launch = sum(a[0].elapsed_time(a[1]) for e in evs for a in e["attn"]) / (args.steps * w.L)
+    ms_attn_launch = sum(hev.ms(a) for e in evs for a in e["attn"]) / (args.steps * w.L)
+    hev.close()
 
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     f_down = 2.0 * w.T * w.d * w.r * w.L
@@ -232,8 +270,9 @@ def run_decode(args, w, layers_timed=None):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    hev = HipEvents()
+    evs = [[hev.pair() for _ in range(L)] for _ in range(args.steps)]
     mk = lambda: torch.cuda.Event(enable_timing=True)
-    evs = [[(mk(), mk()) for _ in range(L)] for _ in range(args.steps)]
     t0, t1 = mk(), mk()
     t0.record()
     for s in range(args.steps):
@@ -242,7 +281,8 @@ def run_decode(args, w, layers_timed=None):
     torch.cuda.synchronize()
     dvl.time_kernel(dvl.KERNEL_ATTENTION)
     ms_step = t0.elapsed_time(t1) / args.steps
-    ms_launch = sum(a.elapsed_time(b) for e in evs for a, b in e) / (args.steps * L)
+    ms_launch = sum(hev.ms(p) for e in evs for p in e) / (args.steps * L)
+    hev.close()
     bytes_layer = configs.bytes_attention(w, layers=1)
     gbs = bytes_layer / (ms_launch * 1e-3) / 1e9
     res = {"ms_per_step": ms_step, "layers": L, "ms_per_layer": ms_step / L,

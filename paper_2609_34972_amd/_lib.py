@@ -114,12 +114,10 @@ def _stream(device: torch.device, stream=None) -> int:
     return s.cuda_stream
 
 
-def time_kernel(kernel: int, begin=None, end=None) -> None:
-    """Bracket every later launch of `kernel` on this thread with two torch.cuda.Event
-    (created with enable_timing=True); time_kernel(kernel) switches the hook off."""
-    b = begin.cuda_event if begin is not None else None
-    e = end.cuda_event if end is not None else None
-    _check(load().dv_time_kernel(kernel, b, e))
+def time_kernel(kernel: int, begin: Optional[int] = None, end: Optional[int] = None) -> None:
+    """Bracket every later launch of `kernel` on this thread with two hipEvent_t handles
+    (raw integers, e.g. from hipEventCreate); time_kernel(kernel) switches the hook off."""
+    _check(load().dv_time_kernel(kernel, begin, end))
 
 
 def build_visual_memory(E: torch.Tensor, Dw: torch.Tensor, Z: torch.Tensor, act: int = ACT_SILU,
