@@ -67,7 +67,7 @@ dv_status hip_status(hipError_t e, const char* what) {
 size_t kv_ws_layer_bytes(int64_t T, int32_t d, int32_t dtype) {
   const size_t mem = (size_t)T * (size_t)d * elem_size(dtype);
   const size_t mem_al = (mem + 255) / 256 * 256;
-  const size_t ssq = (size_t)dv::kv_partials(d, dtype == DV_BF16 ? 1 : 0) * (size_t)T * 4;
+  const size_t ssq = (size_t)dv::kv_partials_max(d) * (size_t)T * 4;
   return mem_al + (ssq + 255) / 256 * 256;
 }
 

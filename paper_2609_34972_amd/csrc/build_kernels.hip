@@ -11,7 +11,12 @@
 //                scaled per row by rsqrt(mean(M_l^2) + eps) in the epilogue
 //                (the RMSNorm factor is a per-row scalar, so it commutes with
 //                the product), stored head-major [B, Hkv, Nv, hd].
+//
+// bf16 runs use the pipelined direct-to-LDS engine of gemm_pipe.hpp (k_*_p kernels, one output
+// row per lane in the epilogue); fp32 runs, and the bf16 up projection when r is not a multiple
+// of 64, use the register-staged engine of gemm_tile.hpp.
 #include "build_kernels.hpp"
+#include "gemm_pipe.hpp"
 #include "gemm_tile.hpp"
 
 namespace dv {
@@ -211,6 +216,201 @@ __global__ __launch_bounds__(C::NT) void k_kv_proj(const typename C::elem* __res
   }
 }
 
+
+// ---------------------------------------------------------------- bf16 pipelined kernels
+
+typedef PipeCfg<128, 128, 2, 2> DownP;  // 2304 x 8192 at LLaVA shapes: 1152 tiles
+typedef PipeCfg<128, 128, 2, 2> UpP;    // K = r is short; two blocks per CU overlap epilogues
+typedef PipeCfg<256, 256, 4, 2> KvP;    // 9216 tiles of 256 x 256 over 32 LLaVA layers
+
+template <typename F>
+__device__ __forceinline__ void store4_bf16(bf16* p, float a, float b, float c, float d, F f) {
+  bf16x4 v = {(bf16)f(a), (bf16)f(b), (bf16)f(c), (bf16)f(d)};
+  *(u32x2*)p = __builtin_bit_cast(u32x2, v);
+}
+
+__device__ __forceinline__ void load4_bf16(const bf16* p, float (&x)[4]) {
+  bf16x4 v = __builtin_bit_cast(bf16x4, *(const u32x2*)p);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] = (float)v[e];
+}
+
+template <int ACT>
+__global__ __launch_bounds__(DownP::NT) void k_down_act_p(const bf16* __restrict__ E,
+                                                          const bf16* __restrict__ Dw,
+                                                          bf16* __restrict__ Z, int T, int d,
+                                                          int L, int r) {
+  typedef DownP C;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int N = L * r;
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const int ldb = d * 2;
+  BufOperand A{buffer_rsrc(E + (int64_t)m0 * d, (int64_t)(T - m0) * ldb),
+               buffer_rsrc(E, 0), 1 << 30, ldb};
+  BufOperand B{buffer_rsrc(Dw + (int64_t)n0 * d, (int64_t)(N - n0) * ldb),
+               buffer_rsrc(Dw, 0), 1 << 30, ldb};
+  f32x16 acc[C::FM][C::FN];
+  pipe_mainloop<C>(A, B, d, (bf16*)smem, acc);
+
+  const int lane = threadIdx.x & 63, wave = wave_index();
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a) {
+    const int row = m0 + wm * C::WM + a * 32 + (lane & 31);
+    if (row >= T) continue;
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
+        if (n >= N) continue;
+        const int l = n / r, j = n - l * r;
+        const f32x16& v = acc[a][b];
+        store4_bf16(Z + ((int64_t)l * T + row) * r + j, v[4 * q], v[4 * q + 1], v[4 * q + 2],
+                    v[4 * q + 3], [](float x) { return ACT == 0 ? silu(x) : gelu(x); });
+      }
+  }
+}
+
+__global__ __launch_bounds__(UpP::NT) void k_up_norm_p(const bf16* __restrict__ E,
+                                                       const bf16* __restrict__ Z,
+                                                       const bf16* __restrict__ Uw,
+                                                       const bf16* __restrict__ gamma,
+                                                       bf16* __restrict__ Mg,
+                                                       float* __restrict__ ssq, int T, int d,
+                                                       int r, int l0) {
+  typedef UpP C;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lz = blockIdx.z, l = l0 + lz;
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const bf16* Zl = Z + (int64_t)l * T * r;
+  const bf16* Ul = Uw + (int64_t)l * d * r;
+  const int ldb = r * 2;
+  BufOperand A{buffer_rsrc(Zl + (int64_t)m0 * r, (int64_t)(T - m0) * ldb), buffer_rsrc(Zl, 0),
+               1 << 30, ldb};
+  BufOperand B{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
+               1 << 30, ldb};
+  f32x16 acc[C::FM][C::FN];
+  pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
+
+  const int lane = threadIdx.x & 63, wave = wave_index();
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const bf16* gl = gamma + (int64_t)l * d;
+  bf16* Ml = Mg + (int64_t)lz * T * d;
+  float* red = (float*)smem;  // [WGN][BM]; the main loop ended with a barrier
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a) {
+    const int rl = wm * C::WM + a * 32 + (lane & 31);
+    const int row = m0 + rl;
+    const bool ok = row < T;
+    float ss = 0.f;
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
+        if (!ok || n >= d) continue;
+        float e[4], g[4];
+        load4_bf16(E + (int64_t)row * d + n, e);
+        load4_bf16(gl + n, g);
+        float m[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          m[u] = acc[a][b][4 * q + u] + e[u];
+          ss += m[u] * m[u];
+        }
+        store4_bf16(Ml + (int64_t)row * d + n, m[0] * g[0], m[1] * g[1], m[2] * g[2], m[3] * g[3],
+                    [](float x) { return x; });
+      }
+    ss += shfl_xor(ss, 32);  // the two lane halves hold the same row
+    if (lane < 32) red[wn * C::BM + rl] = ss;
+  }
+  __syncthreads();
+  const int np = (d + C::BN - 1) / C::BN;
+  for (int rr = threadIdx.x; rr < C::BM; rr += C::NT) {
+    const int row = m0 + rr;
+    if (row < T) {
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < C::WGN; ++w) s += red[w * C::BM + rr];
+      ssq[((int64_t)lz * np + blockIdx.x) * T + row] = s;
+    }
+  }
+}
+
+__global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ Mg,
+                                                       const float* __restrict__ ssq,
+                                                       const bf16* __restrict__ Wk,
+                                                       const bf16* __restrict__ Wv,
+                                                       bf16* __restrict__ Kv, bf16* __restrict__ Vv,
+                                                       int B_, int Nv, int d, int Hkv, int hd,
+                                                       int l0, int np, float eps) {
+  typedef KvP C;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int T = B_ * Nv, kv = Hkv * hd, N = 2 * kv;
+  const int lz = blockIdx.z, l = l0 + lz;
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const bf16* Ml = Mg + (int64_t)lz * T * d;
+  const bf16* Wkl = Wk + (int64_t)l * kv * d;
+  const bf16* Wvl = Wv + (int64_t)l * kv * d;
+  const int ldb = d * 2;
+  BufOperand A{buffer_rsrc(Ml + (int64_t)m0 * d, (int64_t)(T - m0) * ldb), buffer_rsrc(Ml, 0),
+               1 << 30, ldb};
+  BufOperand B;
+  if (n0 < kv) {
+    B = BufOperand{buffer_rsrc(Wkl + (int64_t)n0 * d, (int64_t)(kv - n0) * ldb),
+                   buffer_rsrc(Wvl, (int64_t)kv * ldb), kv - n0, ldb};
+  } else {
+    B = BufOperand{buffer_rsrc(Wvl + (int64_t)(n0 - kv) * d, (int64_t)(N - n0) * ldb),
+                   buffer_rsrc(Wvl, 0), 1 << 30, ldb};
+  }
+  // RMSNorm row scales of this block's rows, finished from the partial sums while the first
+  // operand tiles load; kept in the LDS bytes above the two pipeline stages.
+  float* rs_lds = (float*)(smem + C::LDS_BYTES);
+  {
+    const int rr = threadIdx.x >> 1, half = threadIdx.x & 1;  // two threads per row
+    const int row = m0 + rr;
+    float sum = 0.f;
+    if (row < T)
+      for (int p = half; p < np; p += 2) sum += ssq[((int64_t)lz * np + p) * T + row];
+    sum += __shfl_xor(sum, 1, WAVE);
+    if (half == 0) rs_lds[rr] = rsqrtf(sum / (float)d + eps);
+  }
+  f32x16 acc[C::FM][C::FN];
+  pipe_mainloop<C>(A, B, d, (bf16*)smem, acc);  // its barriers also publish rs_lds
+
+  const int lane = threadIdx.x & 63, wave = wave_index();
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int64_t head_stride = (int64_t)Nv * hd;
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a) {
+    const int rl = wm * C::WM + a * 32 + (lane & 31);
+    const int row = m0 + rl;
+    if (row >= T) continue;
+    const float rs = rs_lds[rl];
+    const int bb = row / Nv, ii = row - bb * Nv;
+    const int64_t tok = ((int64_t)l * B_ + bb) * Hkv * head_stride + (int64_t)ii * hd;
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
+        if (n >= N) continue;
+        bf16* out = n < kv ? Kv : Vv;
+        const int o = n < kv ? n : n - kv;
+        const int h = o / hd, c = o - h * hd;
+        const f32x16& v = acc[a][b];
+        store4_bf16(out + tok + (int64_t)h * head_stride + c, v[4 * q] * rs, v[4 * q + 1] * rs,
+                    v[4 * q + 2] * rs, v[4 * q + 3] * rs, [](float x) { return x; });
+      }
+  }
+}
+
+template <typename K>
+static void allow_lds(K kernel, int bytes) {
+  (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+}
+
 // ---------------------------------------------------------------- launchers
 
 static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
@@ -231,12 +431,58 @@ static hipError_t down_launch(const void* E, const void* Dw, void* Z, int T_, in
 
 hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, int d, int L,
                            int r, int act, int dtype, hipStream_t s, const LaunchEvents& ev) {
-  if (dtype == 1) return down_launch<bf16>(E, Dw, Z, (int)T_, d, L, r, act, s, ev);
+  if (dtype == 1) {
+    typedef DownP C;
+    dim3 grid(cdiv((int64_t)L * r, C::BN), cdiv(T_, C::BM));
+    record(ev.down[0], s);
+    if (act == 0)
+      k_down_act_p<0><<<grid, dim3(C::NT), C::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
+                                                              (bf16*)Z, (int)T_, d, L, r);
+    else
+      k_down_act_p<1><<<grid, dim3(C::NT), C::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
+                                                              (bf16*)Z, (int)T_, d, L, r);
+    record(ev.down[1], s);
+    return hipGetLastError();
+  }
   return down_launch<float>(E, Dw, Z, (int)T_, d, L, r, act, s, ev);
 }
 
-int kv_partials(int d, int dtype) {
-  return dtype == 1 ? cdiv(d, BuildTiles<bf16>::Up::BN) : cdiv(d, BuildTiles<float>::Up::BN);
+int kv_partials(int d, int r, int dtype) {
+  if (dtype == 1) return r % 64 == 0 ? cdiv(d, UpP::BN) : cdiv(d, BuildTiles<bf16>::Up::BN);
+  return cdiv(d, BuildTiles<float>::Up::BN);
+}
+
+int kv_partials_max(int d) { return cdiv(d, 64); }
+
+static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, const void* gamma,
+                                 const void* Wk, const void* Wv, void* Kv, void* Vv, int B_,
+                                 int Nv, int d, int r, int Hkv, int hd, int l0, int nl, float eps,
+                                 void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
+                                 bool first, bool last) {
+  constexpr int kv_lds = KvP::LDS_BYTES + KvP::BM * 4;  // stages + row scales
+  static_assert(KvP::NT == 2 * KvP::BM, "two threads per row finish the row scales");
+  static bool once = [] {
+    allow_lds(k_kv_proj_p, kv_lds);
+    return true;
+  }();
+  (void)once;
+  const int T_ = B_ * Nv;
+  const int np = cdiv(d, UpP::BN);
+  dim3 gu(np, cdiv(T_, UpP::BM), nl);
+  if (first) record(ev.up[0], s);
+  k_up_norm_p<<<gu, dim3(UpP::NT), UpP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Z,
+                                                         (const bf16*)Uw, (const bf16*)gamma,
+                                                         (bf16*)Mg, ssq, T_, d, r, l0);
+  if (last) record(ev.up[1], s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 gk(cdiv(2 * Hkv * hd, KvP::BN), cdiv(T_, KvP::BM), nl);
+  if (first) record(ev.kv[0], s);
+  k_kv_proj_p<<<gk, dim3(KvP::NT), kv_lds, s>>>((const bf16*)Mg, ssq, (const bf16*)Wk,
+                                                         (const bf16*)Wv, (bf16*)Kv, (bf16*)Vv, B_,
+                                                         Nv, d, Hkv, hd, l0, np, eps);
+  if (last) record(ev.kv[1], s);
+  return hipGetLastError();
 }
 
 template <typename T>
@@ -267,6 +513,9 @@ hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const
                              int d, int r, int Hkv, int hd, int l0, int nl, float eps, int dtype,
                              void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
                              bool first, bool last) {
+  if (dtype == 1 && r % 64 == 0)
+    return kv_launch_bf16(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv, hd, l0, nl, eps, Mg,
+                          ssq, s, ev, first, last);
   if (dtype == 1)
     return kv_launch<bf16>(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv, hd, l0, nl, eps,
                            Mg, ssq, s, ev, first, last);

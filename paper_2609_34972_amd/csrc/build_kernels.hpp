@@ -22,8 +22,10 @@ inline void record(hipEvent_t e, hipStream_t s) {
 hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T, int d, int L, int r,
                            int act, int dtype, hipStream_t s, const LaunchEvents& ev);
 
-// Number of fp32 partial sums of squares per row written by the up kernel.
-int kv_partials(int d, int dtype);
+// Number of fp32 partial sums of squares per row written by the up kernel of this call, and
+// the largest count over every variant (used to size the workspace).
+int kv_partials(int d, int r, int dtype);
+int kv_partials_max(int d);
 
 // Layers l0..l0+nl-1: memory, RMSNorm and K/V projection. Mg holds nl*T*d
 // elements of the call dtype and ssq nl*kv_partials(d)*T floats.

@@ -1,0 +1,173 @@
+// Software-pipelined bf16 "NT" GEMM main loop for gfx950:  C[m][n] = sum_k A[m][k] * B[n][k].
+//
+// * Operand tiles go straight from HBM into LDS with buffer_load ... lds (no staging registers).
+//   The buffer resources carry the valid byte range, so rows past the end read as zeros instead
+//   of faulting.
+// * Two 64-deep LDS stages: the loads of tile k+2 are issued as soon as every wave has finished
+//   reading tile k, and the next tile's first fragments are read before the last MFMA group of
+//   the current tile, so one barrier per K tile carries no exposed LDS latency.
+// * 128-byte LDS rows with an XOR swizzle of the 16-byte chunks keyed on (row / 2) mod 8: the
+//   16 rows read together by a fragment load land in 16 distinct bank groups. Lanes of a load
+//   instruction pick the global chunk that belongs at their LDS slot, so the swizzle costs
+//   nothing at load time.
+// * The MFMA operands are swapped (acc = B-fragment x A-fragment), which leaves the transpose
+//   of the 32x32 tile in the accumulators: lane l holds row m = l % 32 of its fragment and four
+//   runs of four consecutive columns. Epilogues therefore see one output row per lane (per-row
+//   scales are per lane) and store 8-byte runs along the row.
+#pragma once
+
+#include "dv_device.hpp"
+
+namespace dv {
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// s_waitcnt immediate (gfx9 encoding): at most `vm` vector-memory and `lgkm` LDS/scalar ops
+// outstanding, export count not waited on.
+constexpr int waitcnt_imm(int vm, int lgkm) {
+  return (vm & 0xF) | ((vm >> 4) << 14) | (0x7 << 4) | ((lgkm & 0xF) << 8);
+}
+
+constexpr int kRawBufferFlags = 0x00020000;  // dword 3 of a raw (unformatted) buffer resource
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int64_t bytes) {
+  const int nr = bytes > 0x7fffffff ? 0x7fffffff : (bytes < 0 ? 0 : (int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nr, kRawBufferFlags);
+}
+
+// One GEMM operand as row ranges of up to two buffers: rows [0, nsplit) come from r0, rows
+// [nsplit, ...) from r1 (row nsplit is r1's first row). Row pitch in bytes.
+struct BufOperand {
+  __amdgpu_buffer_rsrc_t r0, r1;
+  int nsplit;
+  int ld_bytes;
+};
+
+__device__ __forceinline__ int wave_index() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
+template <int BM_, int BN_, int WGM_, int WGN_>
+struct PipeCfg {
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
+  static constexpr int NWAVES = WGM * WGN, NT = WAVE * NWAVES;
+  static constexpr int BK = 64;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
+  static constexpr int FM = WM / 32, FN = WN / 32;
+  static constexpr int A_INS = BM / 8 / NWAVES;  // 8-row (1 KiB) load instructions per wave
+  static constexpr int B_INS = BN / 8 / NWAVES;
+  static constexpr int INS = A_INS + B_INS;
+  static constexpr int STAGE = (BM + BN) * BK;   // bf16 elements per stage
+  static constexpr int LDS_BYTES = 2 * STAGE * 2;
+  static_assert(WM % 32 == 0 && WN % 32 == 0 && A_INS >= 1 && B_INS >= 1, "bad tile");
+};
+
+// Lane byte offset inside an 8-row load block: LDS slot (row r = lane / 8, chunk pc = lane % 8)
+// holds logical chunk pc ^ key(row), key(row) = (row / 2) % 8 = (r / 2) | 4 * (block % 2).
+__device__ __forceinline__ int pipe_lane_offset(int ld_bytes, int odd_block) {
+  const int lane = threadIdx.x & 63, r = lane >> 3, pc = lane & 7;
+  const int key = (r >> 1) | (odd_block << 2);
+  return r * ld_bytes + ((pc ^ key) << 4);
+}
+
+template <class C>
+__device__ __forceinline__ void pipe_issue(const BufOperand& A, const BufOperand& B, int kbytes,
+                                           bf16* stage, int va0, int va1, int vb0, int vb1) {
+  const int wave = wave_index();
+#pragma unroll
+  for (int i = 0; i < C::A_INS; ++i) {
+    const int blk = wave * C::A_INS + i;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(A.r0, (lds_void*)(stage + blk * 512), 16,
+                                             (blk & 1) ? va1 : va0, blk * 8 * A.ld_bytes + kbytes,
+                                             0, 0);
+  }
+  bf16* sb = stage + C::BM * C::BK;
+#pragma unroll
+  for (int i = 0; i < C::B_INS; ++i) {
+    const int blk = wave * C::B_INS + i;
+    const int row = blk * 8;
+    const bool first = row < B.nsplit;
+    const int soff = (first ? row : row - B.nsplit) * B.ld_bytes + kbytes;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(first ? B.r0 : B.r1, (lds_void*)(sb + blk * 512), 16,
+                                             (blk & 1) ? vb1 : vb0, soff, 0, 0);
+  }
+}
+
+__device__ __forceinline__ bf16x8 pipe_frag(const bf16* s, int row, int chunk) {
+  const int pc = chunk ^ ((row >> 1) & 7);
+  return __builtin_bit_cast(bf16x8, *(const u32x4*)(s + row * 64 + pc * 8));
+}
+
+template <class C>
+__device__ __forceinline__ void pipe_frags(const bf16* s, int ks, bf16x8 (&fa)[C::FM],
+                                           bf16x8 (&fb)[C::FN]) {
+  const int lane = threadIdx.x & 63, wave = wave_index();
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int chunk = ks * 2 + (lane >> 5);
+  const bf16* sb = s + C::BM * C::BK;
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a) fa[a] = pipe_frag(s, wm * C::WM + a * 32 + (lane & 31), chunk);
+#pragma unroll
+  for (int b = 0; b < C::FN; ++b) fb[b] = pipe_frag(sb, wn * C::WN + b * 32 + (lane & 31), chunk);
+}
+
+template <class C>
+__device__ __forceinline__ void pipe_mfmas(f32x16 (&acc)[C::FM][C::FN], const bf16x8 (&fa)[C::FM],
+                                           const bf16x8 (&fb)[C::FN]) {
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b) mfma_k16(acc[a][b], fb[b], fa[a]);  // transposed tile
+}
+
+template <int IMM>
+__device__ __forceinline__ void pipe_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(IMM);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Column of accumulator item i of this lane inside its 32x32 fragment (the row is lane % 32):
+// items 4q..4q+3 are columns 8q + 4*(lane/32) + 0..3.
+__device__ __forceinline__ int pipe_col(int lane, int q) { return q * 8 + (lane >> 5) * 4; }
+
+// A: block-tile rows start at A's first row; B likewise. K must be a multiple of 64.
+template <class C>
+__device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOperand& B, int K,
+                                              bf16* lds, f32x16 (&acc)[C::FM][C::FN]) {
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b) acc[a][b] = f32x16{};
+  const int va0 = pipe_lane_offset(A.ld_bytes, 0), va1 = pipe_lane_offset(A.ld_bytes, 1);
+  const int vb0 = pipe_lane_offset(B.ld_bytes, 0), vb1 = pipe_lane_offset(B.ld_bytes, 1);
+  const int nk = K / C::BK;
+  pipe_issue<C>(A, B, 0, lds, va0, va1, vb0, vb1);
+  if (nk > 1) {
+    pipe_issue<C>(A, B, C::BK * 2, lds + C::STAGE, va0, va1, vb0, vb1);
+    pipe_sync<waitcnt_imm(C::INS, 0)>();  // tile 0 landed, tile 1 stays in flight
+  } else {
+    pipe_sync<waitcnt_imm(0, 0)>();
+  }
+  bf16x8 fa[2][C::FM], fb[2][C::FN];
+  pipe_frags<C>(lds, 0, fa[0], fb[0]);
+  for (int kt = 0; kt < nk; ++kt) {
+    bf16* s = lds + (kt & 1) * C::STAGE;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < 3) {
+        pipe_frags<C>(s, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+      } else {
+        // Every wave holds its last fragments of stage s and tile kt+1 has landed: refill s
+        // with tile kt+2 and fetch tile kt+1's first fragments before this tile's last MFMAs.
+        pipe_sync<waitcnt_imm(0, 0)>();
+        if (kt + 2 < nk) pipe_issue<C>(A, B, (kt + 2) * C::BK * 2, s, va0, va1, vb0, vb1);
+        if (kt + 1 < nk) pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
+      }
+      pipe_mfmas<C>(acc, fa[ks & 1], fb[ks & 1]);
+    }
+  }
+}
+
+}  // namespace dv
