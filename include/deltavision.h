@@ -103,7 +103,7 @@ dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, con
  *   Q, O   [B, Nq, Hq, hd]
  *   Kv, Vv [B, Hkv, Nv, hd]   one layer of the visual cache (may be NULL when Nv == 0)
  *   Kt, Vt [B, Hkv, Nkt, hd]  text key / value cache; requires q_pos0 + Nq <= Nkt
- *   scale  softmax scale, usually 1/sqrt(hd)
+ *   scale  softmax scale, finite and > 0, usually 1/sqrt(hd)
  *   ws     split-key partials; may be NULL/0 (then keys are not split). With
  *          dv_text_visual_attention_workspace(...) bytes the call picks its
  *          preferred split; with fewer it uses the largest split that fits.

@@ -207,7 +207,8 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
     return fail(DV_ERR_SHAPE, "key count exceeds 2^30 or B*Nq*Hq exceeds 2^23");
   if ((int64_t)B * Hkv > 65535) return fail(DV_ERR_SHAPE, "B*Hkv=%lld exceeds 65535", (long long)B * Hkv);
   if (hd != 64 && hd != 128) return fail(DV_ERR_UNSUPPORTED, "hd=%d must be 64 or 128", hd);
-  if (!std::isfinite(scale)) return fail(DV_ERR_SHAPE, "scale must be finite");
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(DV_ERR_SHAPE, "scale must be finite and > 0");
   DV_CHECK(need_ptr(Q, "Q"));
   if (Nv > 0) {
     DV_CHECK(need_ptr(Kv, "Kv"));
@@ -218,7 +219,8 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
   DV_CHECK(need_ptr(O, "O"));
   if (ws && !aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
   const dv::AttnPlan plan =
-      dv::plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, ws ? ws_bytes : 0);
+      dv::plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, dtype == DV_BF16 ? 1 : 0,
+                         ws ? ws_bytes : 0);
   dv::AttnArgs a{};
   a.Q = Q;
   a.Kv = Kv;
@@ -240,6 +242,7 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
   a.scale_log2 = scale * 1.4426950408889634f;
   a.splits = plan.splits;
   a.keys_per_split = plan.keys_per_split;
+  a.tiles_per_split = plan.tiles_per_split;
   return hip_status(dv::launch_attention(a, plan, dtype == DV_BF16 ? 1 : 0, (hipStream_t)stream,
                                          g_ev),
                     "dv_text_visual_attention launch");

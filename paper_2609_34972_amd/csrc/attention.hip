@@ -14,9 +14,14 @@
 //   k_attn_decode   one query per sequence: a bandwidth-bound stream over the
 //                   K/V caches with 16-byte loads, dot products reduced across
 //                   the lanes of one key row, and an online softmax.
+//   k_attn_stream   bf16, hd 128 prefill: the same math with K/V tiles loaded straight into
+//                   LDS (range-checked buffer loads, two stages in flight), keys walked as
+//                   visual tiles then text tiles so each tile has one source, and the V^T
+//                   fragment read with two ds_read_b64_tr_b16 transpose loads.
 //   k_attn_combine  log-sum-exp merge of key-split partials.
 #include "attention.hpp"
 #include "dv_device.hpp"
+#include "gemm_pipe.hpp"
 
 #include <math.h>
 
@@ -266,6 +271,523 @@ __global__ __launch_bounds__(NW * 64) void k_attn_prefill(AttnArgs a) {
   }
 }
 
+
+// ------------------------------------------------------------------ streaming prefill (bf16)
+
+namespace stream {
+constexpr int HD = 128;
+constexpr int KT = 64;                    // keys per tile
+constexpr int ROWB = HD * 2;              // bytes per K/V row
+constexpr int TILE_BYTES = KT * ROWB;     // one tensor's tile: 16 KiB
+constexpr int STAGE_BYTES = 2 * TILE_BYTES;
+// Stages: up to two tiles keep loading while one is computed. A wave counts at most 63
+// outstanding loads (6-bit vmcnt), i.e. two tiles of a single-wave block.
+template <int NW> constexpr int stages() { return 3; }
+template <int NW> constexpr int lds_bytes() { return stages<NW>() * STAGE_BYTES; }
+constexpr int BLOCKS_PER_TILE = KT / 4;   // 1 KiB (4-row) load instructions per tensor
+// XOR keys of the 16-byte chunks of a 256-byte LDS row. K rows are read whole-chunk by 16 rows
+// at once (key = row mod 16); V rows are read by the transpose loads as 4 rows x 2 chunks per
+// 16 lanes (key = 2 * (row mod 8) keeps those 8 chunks in distinct bank groups).
+__device__ __forceinline__ int key_k(int row) { return row & 15; }
+__device__ __forceinline__ int key_v(int row) { return (row & 7) << 1; }
+}  // namespace stream
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// Online-softmax step of one tile for the query row of this lane (the two lane halves hold the
+// same row). Scores arrive raw; masked ones are -inf. The running max m (in units of
+// scale*log2 e) is only raised when some row of the wave grew by more than 2^8: between raises
+// p = 2^(s*scale - m) stays below 256, and since the sum and O use the same stale m the result
+// is unchanged while most tiles skip the rescale of O.
+template <int NI, int NCB>
+__device__ __forceinline__ void online_softmax(float (&sv)[NI], float scale_log2, float& m_run,
+                                               float& l_run, f32x16 (&oacc)[NCB]) {
+  float tmax = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) tmax = fmaxf(tmax, sv[i]);
+  tmax = fmaxf(tmax, shfl_xor(tmax, 32)) * scale_log2;
+  const bool grow = tmax > m_run + 8.0f;
+  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+    const float m_new = fmaxf(m_run, tmax);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) oacc[cb] *= alpha;
+  }
+  const float neg_m = -m_run;
+  float psum = 0.f;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const float p = __builtin_amdgcn_exp2f(fmaf(sv[i], scale_log2, neg_m));
+    sv[i] = p;
+    psum += p;
+  }
+  l_run += psum;
+}
+
+// Block-uniform integer that the compiler computes on the vector unit (integer divisions):
+// stating it is uniform keeps load bases and sizes in scalar registers.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Wait until tile t+1 of the pipeline has landed when `ahead` later tiles may stay in flight
+// (never encoding more than the 63 loads vmcnt can count), then synchronise the block.
+template <int INS>
+__device__ __forceinline__ void stream_sync(int ahead) {
+  constexpr int kMaxTiles = 63 / INS;
+  if (ahead > kMaxTiles) ahead = kMaxTiles;
+  if (ahead >= 2) pipe_sync<waitcnt_imm((kMaxTiles >= 2 ? 2 : 0) * INS, 0)>();
+  else if (ahead == 1) pipe_sync<waitcnt_imm(INS, 0)>();
+  else pipe_sync<waitcnt_imm(0, 0)>();
+}
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn_stream(AttnArgs a, int row_blocks) {
+  using namespace stream;
+  constexpr int NS = stages<NW>();
+  constexpr int INS = 2 * BLOCKS_PER_TILE / NW;  // load instructions per wave per tile
+  static_assert(NS - 1 <= 2 && INS <= 63, "stream_sync handles at most two tiles in flight");
+  static_assert(BLOCKS_PER_TILE % NW == 0, "waves must split the tile loads evenly");
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int lane = threadIdx.x & 63, wave = wave_index(), g2 = lane >> 5;
+  const int G = a.Hq / a.Hkv, R = a.Nq * G, n_bg = a.B * a.Hkv;
+
+  // Blocks id and id + 8 run on the same XCD; give them the same (batch, kv-head) so the
+  // row-blocks sharing one K/V stream share that XCD's L2.
+  int rb, bg;
+  {
+    const int id = blockIdx.x, full = (n_bg / 8) * 8 * row_blocks;
+    if (id < full) {
+      rb = (id / 8) % row_blocks;
+      bg = (id % 8) + 8 * (id / (8 * row_blocks));
+    } else {
+      const int r = id - full;
+      rb = r % row_blocks;
+      bg = (n_bg / 8) * 8 + r / row_blocks;
+    }
+  }
+  rb = uni(rb);
+  bg = uni(bg);
+  const int b = uni(bg / a.Hkv), g = bg - b * a.Hkv;
+  const int split = blockIdx.y;
+  const int row0 = rb * 32 * NW;
+  const int my_row = row0 + wave * 32 + (lane & 31);
+  const bool row_ok = my_row < R;
+  const int my_i = row_ok ? my_row / G : 0;
+  const int my_h = g * G + (row_ok ? my_row - my_i * G : 0);
+  const int i_max = uni((min(row0 + 32 * NW, R) - 1) / G);
+  const int text_lim = min(a.Nkt, a.q_pos0 + i_max + 1);  // text keys any row of the block needs
+  const int my_text_last = a.q_pos0 + my_i;                // last text key of my row
+  const int tv = uni((a.Nv + KT - 1) / KT), ntiles = uni(tv + (text_lim + KT - 1) / KT);
+  const int t_begin = split * a.tiles_per_split;
+  const int t_end = min(ntiles, t_begin + a.tiles_per_split);
+
+  const bf16* kvb = (const bf16*)a.Kv + (int64_t)bg * a.Nv * HD;
+  const bf16* vvb = (const bf16*)a.Vv + (int64_t)bg * a.Nv * HD;
+  const bf16* ktb = (const bf16*)a.Kt + (int64_t)bg * a.Nkt * HD;
+  const bf16* vtb = (const bf16*)a.Vt + (int64_t)bg * a.Nkt * HD;
+  const int64_t vis_bytes = (int64_t)a.Nv * ROWB, txt_bytes = (int64_t)text_lim * ROWB;
+
+  // Q^T fragments of my row (B operand of S^T = K Q^T).
+  bf16x8 qf[HD / 16];
+  {
+    const bf16* qrow = (const bf16*)a.Q + (((int64_t)b * a.Nq + my_i) * a.Hq + my_h) * HD;
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+      qf[ks] = row_ok ? __builtin_bit_cast(bf16x8, ld16(qrow + ks * 16 + g2 * 8)) : bf16x8{};
+  }
+
+  // Lane part of a load instruction: row r4 = lane / 16 of a 4-row block, LDS chunk pc.
+  const int r4 = lane >> 4, pc = lane & 15;
+  auto issue = [&](int t, int stage) {
+    const bool vis = t < tv;
+    const int key0 = (vis ? t : t - tv) * KT;
+    unsigned char* sk = smem + stage * STAGE_BYTES;
+    unsigned char* sv = sk + TILE_BYTES;
+    // Select the (uniform) base and size, then build the resources: a select between two
+    // resources would be lowered per lane and force a waterfall loop around every load.
+    const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(vis ? kvb : ktb, vis ? vis_bytes : txt_bytes);
+    const __amdgpu_buffer_rsrc_t rv = buffer_rsrc(vis ? vvb : vtb, vis ? vis_bytes : txt_bytes);
+#pragma unroll
+    for (int i = 0; i < BLOCKS_PER_TILE / NW; ++i) {
+      const int blk = wave * (BLOCKS_PER_TILE / NW) + i;
+      const int row = blk * 4 + r4;
+      const int soff = (key0 + blk * 4) * ROWB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(sk + blk * 1024), 16,
+                                               r4 * ROWB + ((pc ^ key_k(row)) << 4), soff, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(sv + blk * 1024), 16,
+                                               r4 * ROWB + ((pc ^ key_v(row)) << 4), soff, 0, 0);
+    }
+  };
+
+  f32x16 oacc[HD / 32];
+#pragma unroll
+  for (int cb = 0; cb < HD / 32; ++cb) oacc[cb] = f32x16{};
+  float m_run = NEG_BIG, l_run = 0.f;
+
+  // Prologue: fill every stage, then wait for the first tile only.
+  const int nt = t_end - t_begin;
+#pragma unroll
+  for (int j = 0; j < NS; ++j)
+    if (j < nt) issue(t_begin + j, j);
+  stream_sync<INS>(min(NS, nt) - 1);
+
+  // Transpose-load lane roles (fixed for the whole loop): in each 16-lane group, lane L points
+  // at key row (L / 4) of a 4-key group and columns c0 + 4 (L % 4) .. + 3 of it.
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int tr_row = l16 >> 2;
+  const int tr_col = 16 * (grp & 1) + 4 * (l16 & 3);  // plus 32 * cb
+
+  int stage = 0;
+  for (int t = t_begin; t < t_end; ++t) {
+    const unsigned char* sk = smem + stage * STAGE_BYTES;
+    const unsigned char* sv = sk + TILE_BYTES;
+    const bool vis = t < tv;
+    const int key0 = (vis ? t : t - tv) * KT;
+
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      sacc[kb] = f32x16{};
+      const int row = kb * 32 + (lane & 31);
+#pragma unroll
+      for (int ks = 0; ks < HD / 16; ++ks) {
+        const int chunk = ks * 2 + g2;
+        bf16x8 kf = __builtin_bit_cast(
+            bf16x8, *(const u32x4*)(sk + row * ROWB + ((chunk ^ key_k(row)) << 4)));
+        mfma_k16(sacc[kb], kf, qf[ks]);
+      }
+    }
+    float scs[32];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) scs[kb * 16 + i] = sacc[kb][i];
+    if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = key0 + kb * 32 + acc_row(lane, i);
+          const bool ok = vis ? key < a.Nv : (key <= my_text_last && key < text_lim);
+          if (!ok) scs[kb * 16 + i] = -INFINITY;
+        }
+    }
+    online_softmax<32, HD / 32>(scs, a.scale_log2, m_run, l_run, oacc);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sacc[kb][i] = scs[kb * 16 + i];
+
+    // O^T += V^T P^T. For K step (kb, s2) slot e of lane half g2 is key
+    // kb*32 + 16*s2 + (e/4)*8 + 4*g2 + e%4 in both operands; the two transpose loads return
+    // slots 0..3 and 4..7 of V^T for column 32*cb + lane % 32.
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        bf16x8 pf;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[kb][s2 * 8 + e];
+        const int krow = kb * 32 + 16 * s2 + 4 * (grp >> 1) + tr_row;
+#pragma unroll
+        for (int cb = 0; cb < HD / 32; ++cb) {
+          const int col = 32 * cb + tr_col;
+          const int chunk = col >> 3, within = (col & 7) * 2;
+          const unsigned char* p0 = sv + krow * ROWB + ((chunk ^ key_v(krow)) << 4) + within;
+          const unsigned char* p1 =
+              sv + (krow + 8) * ROWB + ((chunk ^ key_v(krow + 8)) << 4) + within;
+          const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p0);
+          const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p1);
+          const s16x4 vv[2] = {v0, v1};
+          bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+          mfma_k16(oacc[cb], vf, pf);
+        }
+      }
+    }
+
+    // Tile t+1 has landed (tiles t+2 .. t+NS-1 may still load) and every wave is done with
+    // this stage: refill it with tile t+NS.
+    stream_sync<INS>(min(NS - 2, t_end - t - 2));
+    if (t + NS < t_end) issue(t + NS, stage);
+    stage = stage + 1 == NS ? 0 : stage + 1;
+  }
+
+  const float l_tot = l_run + shfl_xor(l_run, 32);
+  if (!row_ok) return;
+  const int64_t orow = ((int64_t)b * a.Nq + my_i) * a.Hq + my_h;
+  if (a.splits == 1) {
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    bf16* o = (bf16*)a.O + orow * HD;
+#pragma unroll
+    for (int cb = 0; cb < HD / 32; ++cb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int c = cb * 32 + q4 * 8 + g2 * 4;
+        store4<bf16>(o + c, oacc[cb][q4 * 4] * inv, oacc[cb][q4 * 4 + 1] * inv,
+                     oacc[cb][q4 * 4 + 2] * inv, oacc[cb][q4 * 4 + 3] * inv);
+      }
+  } else {
+    const int64_t rows_total = (int64_t)a.B * a.Nq * a.Hq;
+    float* op = a.Opart + ((int64_t)split * rows_total + orow) * HD;
+#pragma unroll
+    for (int cb = 0; cb < HD / 32; ++cb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int c = cb * 32 + q4 * 8 + g2 * 4;
+        *(f32x4*)(op + c) = f32x4{oacc[cb][q4 * 4], oacc[cb][q4 * 4 + 1], oacc[cb][q4 * 4 + 2],
+                                  oacc[cb][q4 * 4 + 3]};
+      }
+    if (g2 == 0) {
+      float* ml = a.MLpart + ((int64_t)split * rows_total + orow) * 2;
+      ml[0] = m_run;
+      ml[1] = l_tot;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ key-split prefill (bf16)
+//
+// For few query rows per (batch, kv-head) (LLaVA: 64) one block of four waves takes 32 rows
+// and every wave streams a quarter of the 32-key tiles through its own two LDS stages, so all
+// four SIMDs of the CU work and no barrier is needed until the waves merge their partial
+// (max, sum, O) through LDS.
+
+namespace ksplit {
+constexpr int HD = 128;
+constexpr int KT = 32;                      // keys per tile
+constexpr int NWAVE = 4;                    // key groups per block
+constexpr int ROWB = HD * 2;
+constexpr int TILE_BYTES = KT * ROWB;       // 8 KiB per tensor
+constexpr int STAGE_BYTES = 2 * TILE_BYTES;
+constexpr int NS = 2;
+constexpr int WAVE_BYTES = NS * STAGE_BYTES;
+constexpr int LDS_BYTES = NWAVE * WAVE_BYTES;  // 128 KiB; the merge reuses it
+constexpr int INS = 2 * KT / 4;             // 1 KiB load instructions per tile
+constexpr int MPITCH = HD + 4;              // merge rows padded by 16 B: rows fall on distinct banks
+static_assert(NWAVE * 32 * (MPITCH + 2) * 4 <= LDS_BYTES, "merge buffer must fit");
+}  // namespace ksplit
+
+__global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, int row_blocks) {
+  using namespace ksplit;
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int lane = threadIdx.x & 63, wave = wave_index(), g2 = lane >> 5;
+  const int G = a.Hq / a.Hkv, R = a.Nq * G, n_bg = a.B * a.Hkv;
+  int rb, bg;  // blocks id and id + 8 share an XCD: give them the same (batch, kv-head)
+  {
+    const int id = blockIdx.x, full = (n_bg / 8) * 8 * row_blocks;
+    if (id < full) {
+      rb = (id / 8) % row_blocks;
+      bg = (id % 8) + 8 * (id / (8 * row_blocks));
+    } else {
+      const int r = id - full;
+      rb = r % row_blocks;
+      bg = (n_bg / 8) * 8 + r / row_blocks;
+    }
+  }
+  rb = uni(rb);
+  bg = uni(bg);
+  const int b = uni(bg / a.Hkv), g = bg - b * a.Hkv;
+  const int split = blockIdx.y;
+  const int row0 = rb * 32;
+  const int my_row = row0 + (lane & 31);
+  const bool row_ok = my_row < R;
+  const int my_i = row_ok ? my_row / G : 0;
+  const int my_h = g * G + (row_ok ? my_row - my_i * G : 0);
+  const int i_max = uni((min(row0 + 32, R) - 1) / G);
+  const int text_lim = min(a.Nkt, a.q_pos0 + i_max + 1);
+  const int my_text_last = a.q_pos0 + my_i;
+  const int tv = uni((a.Nv + KT - 1) / KT), ntiles = uni(tv + (text_lim + KT - 1) / KT);
+  const int t_begin = split * a.tiles_per_split;
+  const int t_end = min(ntiles, t_begin + a.tiles_per_split);
+
+  const bf16* kvb = (const bf16*)a.Kv + (int64_t)bg * a.Nv * HD;
+  const bf16* vvb = (const bf16*)a.Vv + (int64_t)bg * a.Nv * HD;
+  const bf16* ktb = (const bf16*)a.Kt + (int64_t)bg * a.Nkt * HD;
+  const bf16* vtb = (const bf16*)a.Vt + (int64_t)bg * a.Nkt * HD;
+  const int64_t vis_bytes = (int64_t)a.Nv * ROWB, txt_bytes = (int64_t)text_lim * ROWB;
+
+  bf16x8 qf[HD / 16];
+  {
+    const bf16* qrow = (const bf16*)a.Q + (((int64_t)b * a.Nq + my_i) * a.Hq + my_h) * HD;
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+      qf[ks] = row_ok ? __builtin_bit_cast(bf16x8, ld16(qrow + ks * 16 + g2 * 8)) : bf16x8{};
+  }
+
+  unsigned char* mine = smem + wave * WAVE_BYTES;  // this wave's two stages
+  const int r4 = lane >> 4, pc = lane & 15;
+  auto issue = [&](int t, int stage) {
+    const bool vis = t < tv;
+    const int key0 = (vis ? t : t - tv) * KT;
+    unsigned char* sk = mine + stage * STAGE_BYTES;
+    unsigned char* sv = sk + TILE_BYTES;
+    const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(vis ? kvb : ktb, vis ? vis_bytes : txt_bytes);
+    const __amdgpu_buffer_rsrc_t rv = buffer_rsrc(vis ? vvb : vtb, vis ? vis_bytes : txt_bytes);
+#pragma unroll
+    for (int blk = 0; blk < KT / 4; ++blk) {
+      const int row = blk * 4 + r4;
+      const int soff = (key0 + blk * 4) * ROWB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(sk + blk * 1024), 16,
+                                               r4 * ROWB + ((pc ^ stream::key_k(row)) << 4), soff,
+                                               0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(sv + blk * 1024), 16,
+                                               r4 * ROWB + ((pc ^ stream::key_v(row)) << 4), soff,
+                                               0, 0);
+    }
+  };
+
+  f32x16 oacc[HD / 32];
+#pragma unroll
+  for (int cb = 0; cb < HD / 32; ++cb) oacc[cb] = f32x16{};
+  float m_run = NEG_BIG, l_run = 0.f;
+
+  const int l16 = lane & 15, grp = lane >> 4;
+  const int tr_row = l16 >> 2;
+  const int tr_col = 16 * (grp & 1) + 4 * (l16 & 3);
+
+  // My tiles: t_begin + wave, + NWAVE, ...  Only this wave reads its stages: waits only.
+  int t = t_begin + wave;
+  if (t < t_end) issue(t, 0);
+  if (t + NWAVE < t_end) issue(t + NWAVE, 1);
+  int stage = 0;
+  for (; t < t_end; t += NWAVE) {
+    if (t + NWAVE < t_end) __builtin_amdgcn_s_waitcnt(waitcnt_imm(INS, 0));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+    asm volatile("" ::: "memory");
+    const unsigned char* sk = mine + stage * STAGE_BYTES;
+    const unsigned char* sv = sk + TILE_BYTES;
+    const bool vis = t < tv;
+    const int key0 = (vis ? t : t - tv) * KT;
+
+    f32x16 sacc = f32x16{};
+    {
+      const int row = lane & 31;
+#pragma unroll
+      for (int ks = 0; ks < HD / 16; ++ks) {
+        const int chunk = ks * 2 + g2;
+        bf16x8 kf = __builtin_bit_cast(
+            bf16x8, *(const u32x4*)(sk + row * ROWB + ((chunk ^ stream::key_k(row)) << 4)));
+        mfma_k16(sacc, kf, qf[ks]);
+      }
+    }
+    float scs[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) scs[i] = sacc[i];
+    if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = key0 + acc_row(lane, i);
+        const bool ok = vis ? key < a.Nv : (key <= my_text_last && key < text_lim);
+        if (!ok) scs[i] = -INFINITY;
+      }
+    }
+    online_softmax<16, HD / 32>(scs, a.scale_log2, m_run, l_run, oacc);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sacc[i] = scs[i];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      bf16x8 pf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[s2 * 8 + e];
+      const int krow = 16 * s2 + 4 * (grp >> 1) + tr_row;
+#pragma unroll
+      for (int cb = 0; cb < HD / 32; ++cb) {
+        const int col = 32 * cb + tr_col;
+        const int chunk = col >> 3, within = (col & 7) * 2;
+        const unsigned char* p0 = sv + krow * ROWB + ((chunk ^ stream::key_v(krow)) << 4) + within;
+        const unsigned char* p1 =
+            sv + (krow + 8) * ROWB + ((chunk ^ stream::key_v(krow + 8)) << 4) + within;
+        const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p0);
+        const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p1);
+        const s16x4 vv[2] = {v0, v1};
+        mfma_k16(oacc[cb], __builtin_bit_cast(bf16x8, vv), pf);
+      }
+    }
+    // This stage is consumed (lgkmcnt drained) before it is refilled with tile t + 2*NWAVE.
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));
+    asm volatile("" ::: "memory");
+    if (t + 2 * NWAVE < t_end) issue(t + 2 * NWAVE, stage);
+    stage ^= 1;
+  }
+  const float l_mine = l_run + shfl_xor(l_run, 32);
+
+  // Merge the four key groups: every wave publishes (m, l, O^T) and wave w finishes columns
+  // 32w .. 32w + 31 of the block's 32 rows.
+  __syncthreads();
+  float* red_o = (float*)smem;                        // [NWAVE][32 rows][MPITCH]
+  float* red_ml = red_o + NWAVE * 32 * MPITCH;        // [NWAVE][32 rows][2]
+  {
+    const int rrow = lane & 31;
+    float* o = red_o + (wave * 32 + rrow) * MPITCH;
+#pragma unroll
+    for (int cb = 0; cb < HD / 32; ++cb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int c = cb * 32 + q4 * 8 + g2 * 4;
+        *(f32x4*)(o + c) = f32x4{oacc[cb][q4 * 4], oacc[cb][q4 * 4 + 1], oacc[cb][q4 * 4 + 2],
+                                 oacc[cb][q4 * 4 + 3]};
+      }
+    if (g2 == 0) {
+      red_ml[(wave * 32 + rrow) * 2] = m_run;
+      red_ml[(wave * 32 + rrow) * 2 + 1] = l_mine;
+    }
+  }
+  __syncthreads();
+  const int rrow = lane & 31;
+  float mx = NEG_BIG;
+#pragma unroll
+  for (int w = 0; w < NWAVE; ++w) mx = fmaxf(mx, red_ml[(w * 32 + rrow) * 2]);
+  float lt = 0.f, sc[NWAVE];
+#pragma unroll
+  for (int w = 0; w < NWAVE; ++w) {
+    sc[w] = __builtin_amdgcn_exp2f(red_ml[(w * 32 + rrow) * 2] - mx);
+    lt += red_ml[(w * 32 + rrow) * 2 + 1] * sc[w];
+  }
+  if (!row_ok) return;
+  const int64_t orow = ((int64_t)b * a.Nq + my_i) * a.Hq + my_h;
+  const int cbase = wave * 32 + g2 * 16;  // this lane's 16 columns
+  float out[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) out[e] = 0.f;
+#pragma unroll
+  for (int w = 0; w < NWAVE; ++w) {
+    const float* o = red_o + (w * 32 + rrow) * MPITCH + cbase;
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      const f32x4 v = *(const f32x4*)(o + e4 * 4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) out[e4 * 4 + u] += v[u] * sc[w];
+    }
+  }
+  if (a.splits == 1) {
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    bf16* op = (bf16*)a.O + orow * HD + cbase;
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4)
+      store4<bf16>(op + e4 * 4, out[e4 * 4] * inv, out[e4 * 4 + 1] * inv, out[e4 * 4 + 2] * inv,
+                   out[e4 * 4 + 3] * inv);
+  } else {
+    const int64_t rows_total = (int64_t)a.B * a.Nq * a.Hq;
+    float* op = a.Opart + ((int64_t)split * rows_total + orow) * HD + cbase;
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4)
+      *(f32x4*)(op + e4 * 4) = f32x4{out[e4 * 4], out[e4 * 4 + 1], out[e4 * 4 + 2], out[e4 * 4 + 3]};
+    if (wave == 0 && g2 == 0) {
+      float* ml = a.MLpart + ((int64_t)split * rows_total + orow) * 2;
+      ml[0] = mx;
+      ml[1] = lt;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ decode
 
 template <typename T, int HD, int MAXG>
@@ -439,28 +961,46 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ 
 static inline int64_t cdiv64(int64_t x, int64_t y) { return (x + y - 1) / y; }
 
 AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt, int q_pos0,
-                        size_t ws_bytes) {
+                        int dtype, size_t ws_bytes) {
   AttnPlan p{};
   const int G = Hq / Hkv;
   const int64_t rows_total = (int64_t)B * Nq * Hq;
   const int64_t per_split = rows_total * (int64_t)(hd + 2) * 4;
   const int max_keys = Nv + q_pos0 + Nq;  // keys seen by the last query
+  const int n_bg = B * Hkv;
   p.decode = (Nq == 1 && G <= 8);
-  int units, key_gran;
+  p.stream = !p.decode && dtype == 1 && hd == 128;
+  int64_t units, tiles;
+  int64_t min_blocks = 512;
   if (p.decode) {
     p.nw = 4;
-    units = B * Hkv;
-    key_gran = 64;
+    units = n_bg;
+    tiles = cdiv64(max_keys, 64);
+  } else if (p.stream) {
+    const int R = Nq * G;
+    p.ksplit = R <= 64;
+    if (p.ksplit) {
+      // Few rows: blocks of 32 rows whose four waves split the key tiles (32 keys each).
+      p.nw = 4;
+      p.row_blocks = (int)cdiv64(R, 32);
+      tiles = cdiv64(Nv, 32) + cdiv64(std::min(Nkt, q_pos0 + Nq), 32);
+    } else {
+      // Many rows share each K/V tile: blocks of up to 128 rows (four waves), 64-key tiles.
+      p.nw = R <= 96 ? 2 : 4;
+      p.row_blocks = (int)cdiv64(R, 32 * p.nw);
+      tiles = cdiv64(Nv, 64) + cdiv64(std::min(Nkt, q_pos0 + Nq), 64);
+    }
+    units = (int64_t)n_bg * p.row_blocks;
+    min_blocks = 256;
   } else {
     const int R = Nq * G;
     p.nw = R <= 32 ? 1 : (R <= 64 ? 2 : 4);
     p.row_blocks = (int)cdiv64(R, 32 * p.nw);
-    units = B * Hkv * p.row_blocks;
-    key_gran = 64;
+    units = (int64_t)n_bg * p.row_blocks;
+    tiles = cdiv64(max_keys, 64);
   }
-  // Enough blocks to fill 256 CUs twice, keeping at least two key tiles per split.
-  const int64_t tiles = cdiv64(max_keys, key_gran);
-  int64_t want = cdiv64(512, units);
+  // Split keys only when the blocks do not fill the chip; keep at least two tiles per split.
+  int64_t want = units >= min_blocks ? 1 : cdiv64(min_blocks, units);
   want = std::min<int64_t>(want, std::max<int64_t>(1, tiles / 2));
   want = std::max<int64_t>(1, std::min<int64_t>(want, 64));
   if (want > 1 && per_split > 0) {
@@ -468,17 +1008,19 @@ AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt,
     want = std::min<int64_t>(want, fit);
     if (want < 2) want = 1;
   }
-  p.splits = (int)want;
-  const int64_t tiles_per_split = cdiv64(tiles, p.splits);
-  p.keys_per_split = (int)(tiles_per_split * key_gran);
+  const int64_t tiles_per_split = cdiv64(tiles, want);
+  p.tiles_per_split = (int)tiles_per_split;
+  p.keys_per_split = (int)(tiles_per_split * 64);
   p.splits = (int)cdiv64(tiles, tiles_per_split);  // drop empty trailing splits
   p.ws_needed = p.splits > 1 ? (size_t)(p.splits * per_split) : 0;
   return p;
 }
 
 size_t attention_workspace(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt) {
-  AttnPlan p = plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, Nkt - Nq, (size_t)-1);
-  return p.ws_needed;
+  // The largest need over both dtypes and every valid q_pos0 (more keys never mean fewer splits).
+  const AttnPlan p0 = plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, Nkt - Nq, 0, (size_t)-1);
+  const AttnPlan p1 = plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, Nkt - Nq, 1, (size_t)-1);
+  return std::max(p0.ws_needed, p1.ws_needed);
 }
 
 template <typename T, int HD>
@@ -496,6 +1038,36 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
       k_attn_decode<T, HD, 4><<<grid, dim3(256), 0, s>>>(a);
     else
       k_attn_decode<T, HD, 8><<<grid, dim3(256), 0, s>>>(a);
+  } else if (p.stream) {
+    if constexpr (sizeof(T) == 2 && HD == 128) {
+      static bool once = [] {
+        (void)hipFuncSetAttribute((const void*)k_attn_stream<1>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<1>());
+        (void)hipFuncSetAttribute((const void*)k_attn_stream<2>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<2>());
+        (void)hipFuncSetAttribute((const void*)k_attn_stream<4>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<4>());
+        return true;
+      }();
+      (void)once;
+      dim3 grid(a.B * a.Hkv * p.row_blocks, p.splits);
+      if (p.ksplit) {
+        static bool once_k = [] {
+          (void)hipFuncSetAttribute((const void*)k_attn_ksplit,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, ksplit::LDS_BYTES);
+          return true;
+        }();
+        (void)once_k;
+        k_attn_ksplit<<<grid, dim3(ksplit::NWAVE * 64), ksplit::LDS_BYTES, s>>>(a, p.row_blocks);
+      } else if (p.nw == 1)
+        k_attn_stream<1><<<grid, dim3(64), stream::lds_bytes<1>(), s>>>(a, p.row_blocks);
+      else if (p.nw == 2)
+        k_attn_stream<2><<<grid, dim3(128), stream::lds_bytes<2>(), s>>>(a, p.row_blocks);
+      else
+        k_attn_stream<4><<<grid, dim3(256), stream::lds_bytes<4>(), s>>>(a, p.row_blocks);
+    } else {
+      return hipErrorInvalidValue;  // the planner only picks this kernel for bf16, hd 128
+    }
   } else {
     dim3 grid(p.row_blocks, a.B * a.Hkv, p.splits);
     if (p.nw == 1)

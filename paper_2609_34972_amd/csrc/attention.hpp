@@ -23,10 +23,14 @@ struct AttnArgs {
   int B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0;
   float scale_log2;  // softmax scale times log2(e)
   int splits, keys_per_split;
+  int tiles_per_split;  // bf16 hd-128 prefill: key tiles of 64 per split
 };
 
 struct AttnPlan {
   bool decode;         // one query per sequence: the bandwidth-bound kernel
+  bool stream;         // bf16 hd-128 prefill: direct-to-LDS streaming kernel
+  bool ksplit;         // (stream) few rows per kv-head: four waves split the keys of 32 rows
+  int tiles_per_split;  // (stream) 64-key tiles per split
   int nw;              // waves per block (prefill)
   int row_blocks;      // blocks along the packed (query, head) rows (prefill)
   int splits;          // key splits merged by a log-sum-exp combine
@@ -35,7 +39,7 @@ struct AttnPlan {
 };
 
 AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt, int q_pos0,
-                        size_t ws_bytes);
+                        int dtype, size_t ws_bytes);
 size_t attention_workspace(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt);
 hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int dtype, hipStream_t s,
                             const LaunchEvents& ev);

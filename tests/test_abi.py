@@ -116,7 +116,8 @@ def attn_call(lib, ws=None, ws_bytes=0, **over):
     (dict(Vt=FAKE + 4), ALIGN),
     (dict(B=0), SHAPE), (dict(Nq=0), SHAPE), (dict(Nv=-1), SHAPE), (dict(q0=-1), SHAPE),
     (dict(Hq=6, Hkv=4), SHAPE), (dict(q0=1), SHAPE), (dict(Nkt=15), SHAPE),
-    (dict(scale=float("inf")), SHAPE), (dict(B=70000, Hkv=1, Hq=1), SHAPE),
+    (dict(scale=float("inf")), SHAPE), (dict(scale=0.0), SHAPE), (dict(scale=-0.5), SHAPE),
+    (dict(B=70000, Hkv=1, Hq=1), SHAPE),
     (dict(hd=32), UNSUP), (dict(hd=256), UNSUP), (dict(dt=3), UNSUP),
 ])
 def test_text_visual_attention_rejects(lib, kw, code):
