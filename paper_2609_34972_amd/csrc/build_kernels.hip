@@ -222,6 +222,11 @@ __global__ __launch_bounds__(C::NT) void k_kv_proj(const typename C::elem* __res
 typedef PipeCfg<128, 128, 2, 2> DownP;  // 2304 x 8192 at LLaVA shapes: 1152 tiles
 typedef PipeCfg<128, 128, 2, 2> UpP;    // K = r is short; two blocks per CU overlap epilogues
 typedef PipeCfg<256, 256, 4, 2> KvP;    // 9216 tiles of 256 x 256 over 32 LLaVA layers
+// K/V epilogue staging: per wave 64 rows of 128 bf16, rows padded by 16 B.
+constexpr int kKvEpiPitch = KvP::WN * 2 + 16;
+constexpr int kKvEpiBytes = KvP::NWAVES * KvP::WM * kKvEpiPitch;
+constexpr int kKvRsOffset = KvP::LDS_BYTES > kKvEpiBytes ? KvP::LDS_BYTES : kKvEpiBytes;
+constexpr int kKvLdsBytes = kKvRsOffset + KvP::BM * 4;  // + row scales
 
 template <typename F>
 __device__ __forceinline__ void store4_bf16(bf16* p, float a, float b, float c, float d, F f) {
@@ -366,7 +371,7 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
   }
   // RMSNorm row scales of this block's rows, finished from the partial sums while the first
   // operand tiles load; kept in the LDS bytes above the two pipeline stages.
-  float* rs_lds = (float*)(smem + C::LDS_BYTES);
+  float* rs_lds = (float*)(smem + kKvRsOffset);
   {
     const int rr = threadIdx.x >> 1, half = threadIdx.x & 1;  // two threads per row
     const int row = m0 + rr;
@@ -379,30 +384,46 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
   f32x16 acc[C::FM][C::FN];
   pipe_mainloop<C>(A, B, d, (bf16*)smem, acc);  // its barriers also publish rs_lds
 
+  // Epilogue through LDS: every wave writes its scaled 64 x 128 tile as bf16 rows (pitch padded
+  // by 16 B so the 32 rows written together hit distinct banks), then stores whole 16-byte
+  // pieces: 16 lanes cover one 256-byte row, which lies inside one head of Kv or Vv.
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
-  const int64_t head_stride = (int64_t)Nv * hd;
+  constexpr int EP = kKvEpiPitch;  // bytes per staged row
+  unsigned char* ep = smem + wave * (C::WM * EP);
+  __syncthreads();  // every wave is done with the pipeline stages
 #pragma unroll
   for (int a = 0; a < C::FM; ++a) {
-    const int rl = wm * C::WM + a * 32 + (lane & 31);
-    const int row = m0 + rl;
-    if (row >= T) continue;
-    const float rs = rs_lds[rl];
-    const int bb = row / Nv, ii = row - bb * Nv;
-    const int64_t tok = ((int64_t)l * B_ + bb) * Hkv * head_stride + (int64_t)ii * hd;
+    const int rw = a * 32 + (lane & 31);  // row inside the wave tile
+    const float rs = rs_lds[wm * C::WM + rw];
 #pragma unroll
     for (int b = 0; b < C::FN; ++b)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
-        if (n >= N) continue;
-        bf16* out = n < kv ? Kv : Vv;
-        const int o = n < kv ? n : n - kv;
-        const int h = o / hd, c = o - h * hd;
         const f32x16& v = acc[a][b];
-        store4_bf16(out + tok + (int64_t)h * head_stride + c, v[4 * q] * rs, v[4 * q + 1] * rs,
-                    v[4 * q + 2] * rs, v[4 * q + 3] * rs, [](float x) { return x; });
+        bf16x4 o = {(bf16)(v[4 * q] * rs), (bf16)(v[4 * q + 1] * rs), (bf16)(v[4 * q + 2] * rs),
+                    (bf16)(v[4 * q + 3] * rs)};
+        *(u32x2*)(ep + rw * EP + (b * 32 + pipe_col(lane, q)) * 2) = __builtin_bit_cast(u32x2, o);
       }
+  }
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));  // this wave's LDS writes landed
+  const int64_t head_stride = (int64_t)Nv * hd;
+  constexpr int LPR = C::WN / 8;        // lanes per row (8 bf16 each)
+  constexpr int RPI = WAVE / LPR;       // rows per store instruction
+  const int cpiece = (lane % LPR) * 8;  // first column of this lane's piece
+#pragma unroll 4
+  for (int r0 = 0; r0 < C::WM; r0 += RPI) {
+    const int rw = r0 + lane / LPR;
+    const int row = m0 + wm * C::WM + rw;
+    const int n = n0 + wn * C::WN + cpiece;
+    if (row >= T || n >= N) continue;
+    const u32x4 v = *(const u32x4*)(ep + rw * EP + cpiece * 2);
+    const int bb = row / Nv, ii = row - bb * Nv;
+    bf16* out = n < kv ? Kv : Vv;
+    const int o = n < kv ? n : n - kv;
+    const int h = o / hd, c = o - h * hd;
+    *(u32x4*)(out + ((int64_t)l * B_ + bb) * Hkv * head_stride + (int64_t)h * head_stride +
+              (int64_t)ii * hd + c) = v;
   }
 }
 
@@ -459,7 +480,7 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
                                  int Nv, int d, int r, int Hkv, int hd, int l0, int nl, float eps,
                                  void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
                                  bool first, bool last) {
-  constexpr int kv_lds = KvP::LDS_BYTES + KvP::BM * 4;  // stages + row scales
+  constexpr int kv_lds = kKvLdsBytes;  // stages (or epilogue staging) + row scales
   static_assert(KvP::NT == 2 * KvP::BM, "two threads per row finish the row scales");
   static bool once = [] {
     allow_lds(k_kv_proj_p, kv_lds);

@@ -166,6 +166,16 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
         if (kt + 1 < nk) pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
       }
       pipe_mfmas<C>(acc, fa[ks & 1], fb[ks & 1]);
+      if (ks < 3) {
+        // Issue order: two MFMAs, then each fragment read of the next K step followed by one
+        // MFMA, so the LDS reads overlap the matrix pipe instead of bunching up.
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+#pragma unroll
+        for (int i = 0; i < C::FM + C::FN; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+      }
     }
   }
 }
