@@ -93,6 +93,24 @@ dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, con
                                void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Recurrent adapter (Section 3.1, Eq. 6) and the visual K/V projection (Section 3.2, Eq. 7) of
+ * every layer in one call:
+ *     M_{-1} = E,   M_l = M_{l-1} + phi(M_{l-1} D_l) U_l,   l = 0 .. L-1,
+ *     Kv_l, Vv_l = RMSNorm(M_l; gamma_l, eps) Wk[l]^T, ... Wv[l]^T   (head-major, as above).
+ * Layer l's down projection needs layer l-1's memory, so the layers run in order; the
+ * layer-to-layer state is kept in fp32 in the workspace for both dtypes.
+ *   E, Dw, Uw, gamma, Wk, Wv, Kv, Vv   as for dv_build_visual_memory / dv_project_visual_kv
+ *   act   dv_act
+ *   ws    at least dv_recurrent_visual_kv_workspace(B*Nv, d, L, r, dtype) bytes
+ */
+size_t dv_recurrent_visual_kv_workspace(int64_t T, int32_t d, int32_t L, int32_t r, int32_t dtype);
+dv_status dv_recurrent_visual_kv(const void* E, const void* Dw, const void* Uw, const void* gamma,
+                                 const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
+                                 int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
+                                 int32_t hd, int32_t act, float eps, int32_t dtype, void* ws,
+                                 size_t ws_bytes, void* stream);
+
+/*
  * Text-query attention of one layer over [visual; text] keys (Section 3.2,
  * Eq. 9; visual tokens precede the text, Section 2 Eq. 2):
  *     O[b,i,h,:] = sum_j softmax_j( scale * <Q[b,i,h,:], K_j> ) V_j
@@ -118,9 +136,11 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
 
 /*
  * Profiling hook. Kernels of the library, as named by dv_kernel:
- *   DV_KERNEL_DOWN       the all-layer down-projection of dv_build_visual_memory
+ *   DV_KERNEL_DOWN       the all-layer down-projection of dv_build_visual_memory, or the
+ *                        whole per-layer adapter chain of dv_recurrent_visual_kv
  *   DV_KERNEL_UP         the up-projection + residual of dv_project_visual_kv
- *   DV_KERNEL_KV         the RMSNorm-scaled K/V projection of dv_project_visual_kv
+ *   DV_KERNEL_KV         the RMSNorm-scaled K/V projection of dv_project_visual_kv and
+ *                        dv_recurrent_visual_kv
  *   DV_KERNEL_ATTENTION  the main attention kernel of dv_text_visual_attention
  *                        (without the split-merge kernel)
  * After dv_time_kernel(k, begin, end) with two hipEvent_t handles, every launch

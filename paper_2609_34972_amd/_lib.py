@@ -31,6 +31,8 @@ EXPORTS = (
     "dv_last_error",
     "dv_abi_version",
     "dv_time_kernel",
+    "dv_recurrent_visual_kv_workspace",
+    "dv_recurrent_visual_kv",
 )
 
 KERNEL_DOWN, KERNEL_UP, KERNEL_KV, KERNEL_ATTENTION = 0, 1, 2, 3
@@ -76,6 +78,10 @@ def load() -> ctypes.CDLL:
         lib.dv_abi_version.restype = i32
         lib.dv_time_kernel.argtypes = [i32, vp, vp]
         lib.dv_time_kernel.restype = i32
+        lib.dv_recurrent_visual_kv_workspace.argtypes = [i64, i32, i32, i32, i32]
+        lib.dv_recurrent_visual_kv_workspace.restype = sz
+        lib.dv_recurrent_visual_kv.argtypes = [vp] * 8 + [i32] * 8 + [f32, i32, vp, sz, vp]
+        lib.dv_recurrent_visual_kv.restype = i32
         _lib = lib
         return lib
 
@@ -158,6 +164,32 @@ def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, l0: int = 0,
                                        _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, l0, nl,
                                        float(eps), code, _ptr(ws), ws.numel(),
                                        _stream(E.device, stream)))
+    return Kv, Vv
+
+
+def recurrent_visual_kv_workspace(T: int, d: int, L: int, r: int, dtype: torch.dtype) -> int:
+    code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
+    return int(load().dv_recurrent_visual_kv_workspace(T, d, L, r, code))
+
+
+def recurrent_visual_kv(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, act: int = ACT_SILU,
+                        ws: Optional[torch.Tensor] = None, stream=None):
+    """Recurrent adapter (Eq. 6) and K/V of every layer into Kv, Vv [L,B,Hkv,Nv,hd]."""
+    L, B, Hkv, Nv, hd = Kv.shape
+    T, d = E.shape
+    r = Dw.shape[1]
+    if (T != B * Nv or tuple(Dw.shape) != (L, r, d) or tuple(Uw.shape) != (L, d, r)
+            or tuple(gamma.shape) != (L, d) or tuple(Wk.shape) != (L, Hkv * hd, d)
+            or Wv.shape != Wk.shape or Vv.shape != Kv.shape):
+        raise ValueError("shape mismatch in recurrent_visual_kv")
+    code = _dtype_code(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv)
+    if ws is None:
+        ws = torch.empty(recurrent_visual_kv_workspace(T, d, L, r, E.dtype), dtype=torch.uint8,
+                         device=E.device)
+    _check(load().dv_recurrent_visual_kv(_ptr(E), _ptr(Dw), _ptr(Uw), _ptr(gamma), _ptr(Wk),
+                                         _ptr(Wv), _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, act,
+                                         float(eps), code, _ptr(ws), ws.numel(),
+                                         _stream(E.device, stream)))
     return Kv, Vv
 
 

@@ -181,6 +181,50 @@ dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, con
   return ok();
 }
 
+size_t dv_recurrent_visual_kv_workspace(int64_t T, int32_t d, int32_t L, int32_t r,
+                                        int32_t dtype) {
+  if (T <= 0 || d <= 0 || L <= 0 || r <= 0 || (dtype != DV_F32 && dtype != DV_BF16)) return 0;
+  return dv::recurrent_layout(T, d, L, r, dtype == DV_BF16 ? 1 : 0).bytes;
+}
+
+dv_status dv_recurrent_visual_kv(const void* E, const void* Dw, const void* Uw, const void* gamma,
+                                 const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
+                                 int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
+                                 int32_t hd, int32_t act, float eps, int32_t dtype, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  DV_CHECK(check_dtype(dtype));
+  if (B <= 0 || Nv <= 0 || d <= 0 || L <= 0 || r <= 0 || Hkv <= 0 || hd <= 0)
+    return fail(DV_ERR_SHAPE, "sizes must be positive (B=%d Nv=%d d=%d L=%d r=%d Hkv=%d hd=%d)", B,
+                Nv, d, L, r, Hkv, hd);
+  const int64_t T = (int64_t)B * Nv;
+  if (T > kMaxTokens || (int64_t)2 * Hkv * hd > INT32_MAX || L > 65535)
+    return fail(DV_ERR_SHAPE, "B*Nv=%lld exceeds %lld (or L > 65535)", (long long)T,
+                (long long)kMaxTokens);
+  if (d % 64 != 0) return fail(DV_ERR_UNSUPPORTED, "d=%d must be a multiple of 64", d);
+  if (r % 16 != 0) return fail(DV_ERR_UNSUPPORTED, "r=%d must be a multiple of 16", r);
+  if (hd != 64 && hd != 128) return fail(DV_ERR_UNSUPPORTED, "hd=%d must be 64 or 128", hd);
+  if (act != DV_ACT_SILU && act != DV_ACT_GELU)
+    return fail(DV_ERR_UNSUPPORTED, "act=%d is not DV_ACT_SILU or DV_ACT_GELU", act);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(DV_ERR_SHAPE, "eps must be finite and >= 0");
+  DV_CHECK(need_ptr(E, "E"));
+  DV_CHECK(need_ptr(Dw, "Dw"));
+  DV_CHECK(need_ptr(Uw, "Uw"));
+  DV_CHECK(need_ptr(gamma, "gamma"));
+  DV_CHECK(need_ptr(Wk, "Wk"));
+  DV_CHECK(need_ptr(Wv, "Wv"));
+  DV_CHECK(need_ptr(Kv, "Kv"));
+  DV_CHECK(need_ptr(Vv, "Vv"));
+  const dv::RecLayout w = dv::recurrent_layout(T, d, L, r, dtype == DV_BF16 ? 1 : 0);
+  if (!ws || ws_bytes < w.bytes)
+    return fail(DV_ERR_WORKSPACE, "workspace of %zu bytes is below the required %zu",
+                ws ? ws_bytes : (size_t)0, w.bytes);
+  if (!aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
+  return hip_status(dv::launch_recurrent(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv, B, Nv, d, L, r, Hkv,
+                                         hd, act, eps, dtype == DV_BF16 ? 1 : 0, ws, w,
+                                         (hipStream_t)stream, g_ev),
+                    "dv_recurrent_visual_kv launch");
+}
+
 size_t dv_text_visual_attention_workspace(int32_t B, int32_t Hq, int32_t Hkv, int32_t hd,
                                           int32_t Nv, int32_t Nq, int32_t Nkt) {
   if (B <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || (hd != 64 && hd != 128) || Nv < 0 ||

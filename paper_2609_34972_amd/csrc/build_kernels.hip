@@ -475,6 +475,34 @@ int kv_partials(int d, int r, int dtype) {
 
 int kv_partials_max(int d) { return cdiv(d, 64); }
 
+hipError_t launch_kv_only(const void* Mg, const float* ssq, const void* Wk, const void* Wv,
+                          void* Kv, void* Vv, int B_, int Nv, int d, int Hkv, int hd, int l0, int nl,
+                          int np, float eps, int dtype, hipStream_t s, const LaunchEvents& ev) {
+  const int T_ = B_ * Nv;
+  if (dtype == 1) {
+    static bool once = [] {
+      allow_lds(k_kv_proj_p, kKvLdsBytes);
+      return true;
+    }();
+    (void)once;
+    dim3 gk(cdiv(2 * Hkv * hd, KvP::BN), cdiv(T_, KvP::BM), nl);
+    record(ev.kv[0], s);
+    k_kv_proj_p<<<gk, dim3(KvP::NT), kKvLdsBytes, s>>>((const bf16*)Mg, ssq, (const bf16*)Wk,
+                                                        (const bf16*)Wv, (bf16*)Kv, (bf16*)Vv, B_,
+                                                        Nv, d, Hkv, hd, l0, np, eps);
+    record(ev.kv[1], s);
+    return hipGetLastError();
+  }
+  typedef typename BuildTiles<float>::KV CK;
+  dim3 gk(cdiv(2 * Hkv * hd, CK::BN), cdiv(T_, CK::BM), nl);
+  record(ev.kv[0], s);
+  k_kv_proj<CK><<<gk, dim3(CK::NT), CK::LDS_BYTES, s>>>((const float*)Mg, ssq, (const float*)Wk,
+                                                         (const float*)Wv, (float*)Kv, (float*)Vv,
+                                                         B_, Nv, d, Hkv, hd, l0, np, eps);
+  record(ev.kv[1], s);
+  return hipGetLastError();
+}
+
 static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, const void* gamma,
                                  const void* Wk, const void* Wv, void* Kv, void* Vv, int B_,
                                  int Nv, int d, int r, int Hkv, int hd, int l0, int nl, float eps,

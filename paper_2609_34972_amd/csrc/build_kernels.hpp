@@ -2,7 +2,11 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
+
+#include <algorithm>
+#include <type_traits>
 
 namespace dv {
 
@@ -34,5 +38,26 @@ hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const
                              int d, int r, int Hkv, int hd, int l0, int nl, float eps, int dtype,
                              void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
                              bool first_group, bool last_group);
+
+// K/V projection alone (Eq. 7) for layers l0..l0+nl-1 from a prepared workspace: Mg holds
+// M_l * gamma_l for each layer of the range (call dtype) and ssq np partial sums of M_l^2 per row.
+hipError_t launch_kv_only(const void* Mg, const float* ssq, const void* Wk, const void* Wv,
+                          void* Kv, void* Vv, int B, int Nv, int d, int Hkv, int hd, int l0, int nl,
+                          int np, float eps, int dtype, hipStream_t s, const LaunchEvents& ev);
+
+// Workspace layout of the recurrent adapter (byte offsets, 256-aligned).
+struct RecLayout {
+  size_t mg, ssq, state, op, z, part, bytes;
+  int np;      // RMSNorm partial sums per row
+  int splits;  // split-K factor of the per-layer down projection
+  int kchunk;  // reduction length of one split (a multiple of the K tile)
+};
+RecLayout recurrent_layout(int64_t T, int d, int L, int r, int dtype);
+
+// Recurrent adapter (Eq. 6) for all L layers followed by the K/V projection of every layer.
+hipError_t launch_recurrent(const void* E, const void* Dw, const void* Uw, const void* gamma,
+                            const void* Wk, const void* Wv, void* Kv, void* Vv, int B, int Nv,
+                            int d, int L, int r, int Hkv, int hd, int act, float eps, int dtype,
+                            void* ws, const RecLayout& w, hipStream_t s, const LaunchEvents& ev);
 
 }  // namespace dv

@@ -135,3 +135,30 @@ def test_attention_workspace_query(lib):
     # Decode over 2048 (batch, head) streams fills the chip without a split.
     assert lib.dv_text_visual_attention_workspace(64, 32, 32, 128, 576, 1, 513) == 0
     assert lib.dv_text_visual_attention_workspace(1, 6, 4, 128, 10, 4, 4) == 0  # invalid GQA
+
+
+def rec_call(lib, ws=FAKE, ws_bytes=None, **over):
+    a = dict(E=FAKE, Dw=FAKE, Uw=FAKE, g=FAKE, Wk=FAKE, Wv=FAKE, Kv=FAKE, Vv=FAKE, B=1, Nv=64,
+             d=256, L=4, r=16, Hkv=4, hd=64, act=0, eps=1e-5, dt=F32)
+    a.update(over)
+    if ws_bytes is None:
+        ws_bytes = lib.dv_recurrent_visual_kv_workspace(a["B"] * a["Nv"], a["d"], a["L"], a["r"], a["dt"])
+    return lib.dv_recurrent_visual_kv(a["E"], a["Dw"], a["Uw"], a["g"], a["Wk"], a["Wv"], a["Kv"],
+                                      a["Vv"], a["B"], a["Nv"], a["d"], a["L"], a["r"], a["Hkv"],
+                                      a["hd"], a["act"], a["eps"], a["dt"], ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(E=None), NULL), (dict(Dw=None), NULL), (dict(Vv=None), NULL), (dict(Uw=FAKE + 2), ALIGN),
+    (dict(B=0), SHAPE), (dict(L=0), SHAPE), (dict(eps=-1.0), SHAPE),
+    (dict(hd=32), UNSUP), (dict(d=100), UNSUP), (dict(r=12), UNSUP), (dict(act=3), UNSUP),
+    (dict(dt=4), UNSUP), (dict(ws=None), WS), (dict(ws_bytes=1024), WS), (dict(ws=FAKE + 8), ALIGN),
+])
+def test_recurrent_visual_kv_rejects(lib, kw, code):
+    assert rec_call(lib, **kw) == code
+
+
+def test_recurrent_workspace_grows_with_layers(lib):
+    a = lib.dv_recurrent_visual_kv_workspace(2304, 4096, 8, 256, BF16)
+    b = lib.dv_recurrent_visual_kv_workspace(2304, 4096, 32, 256, BF16)
+    assert 0 < a < b and lib.dv_recurrent_visual_kv_workspace(0, 4096, 8, 256, BF16) == 0
