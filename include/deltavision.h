@@ -111,6 +111,31 @@ dv_status dv_recurrent_visual_kv(const void* E, const void* Dw, const void* Uw, 
                                  size_t ws_bytes, void* stream);
 
 /*
+ * Layer-wise adapter skipping (appendix on adapter skipping, Tables 14 and 15): the
+ * embedding adapter (Eq. 4-5) and the K/V projection (Eq. 7) run only for the layers
+ * with keep[l] != 0. A skipped layer gets no visual keys at all (its attention runs
+ * with Nv = 0, the text-only case of Eq. 18), so the caches hold only the kept layers,
+ * packed in layer order: cache slot j is the j-th kept layer.
+ *   keep    HOST array of L bytes (not device memory), read during the call only
+ *   E, Dw, Uw, gamma, Wk, Wv   full L-layer weights as for dv_build_visual_memory /
+ *           dv_project_visual_kv
+ *   Kv, Vv  [nkeep, B, Hkv, Nv, hd], nkeep = number of nonzero keep bytes; may be
+ *           NULL when nkeep == 0 (then nothing is launched and DV_OK is returned)
+ *   ws      holds Z of the kept layers plus the projection workspace: at least
+ *           dv_kept_visual_kv_workspace(B*Nv, d, r, 1, dtype) bytes; with
+ *           dv_kept_visual_kv_workspace(B*Nv, d, r, nkeep, dtype) bytes every kept layer
+ *           is projected in one launch per contiguous run of kept layers.
+ * Kept layer l gives bit-identical K/V to dv_project_visual_kv for that layer (same
+ * kernels, same arithmetic order).
+ */
+size_t dv_kept_visual_kv_workspace(int64_t T, int32_t d, int32_t r, int32_t nkeep, int32_t dtype);
+dv_status dv_kept_visual_kv(const void* E, const void* Dw, const void* Uw, const void* gamma,
+                            const void* Wk, const void* Wv, const uint8_t* keep, void* Kv,
+                            void* Vv, int32_t B, int32_t Nv, int32_t d, int32_t L, int32_t r,
+                            int32_t Hkv, int32_t hd, int32_t act, float eps, int32_t dtype,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Text-query attention of one layer over [visual; text] keys (Section 3.2,
  * Eq. 9; visual tokens precede the text, Section 2 Eq. 2):
  *     O[b,i,h,:] = sum_j softmax_j( scale * <Q[b,i,h,:], K_j> ) V_j

@@ -175,17 +175,42 @@ def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, B: int, Nv: int, Hkv: int, hd: in
 
 
 def pipeline(E, Dw, Uw, gamma, Wk, Wv, Q, Kt, Vt, B: int, Nv: int, Hkv: int, hd: int, eps: float,
-             act_kind: int, q_pos0: int = 0, scale: Optional[float] = None, recurrent: bool = False):
+             act_kind: int, q_pos0: int = 0, scale: Optional[float] = None, recurrent: bool = False,
+             keep=None):
     """The whole path: memories (Eq. 5 or 6) -> visual K/V (Eq. 7) -> text attention (Eq. 9).
 
-    Q, Kt, Vt carry a leading layer axis. Returns (Z or None, Kv, Vv, O)."""
+    Q, Kt, Vt carry a leading layer axis. Returns (Z or None, Kv, Vv, O).
+
+    keep: optional per-layer flags for layer-wise adapter skipping (appendix on adapter
+    skipping, Tables 14-15; defined there for the embedding adapter). A skipped layer has no
+    visual memory, so its text queries attend to text keys only (Eq. 18). Z, Kv and Vv then
+    hold the kept layers in layer order; O still has every layer."""
+    L = Dw.shape[0]
+    if keep is None:
+        kept = list(range(L))
+    else:
+        if recurrent:
+            raise ValueError("adapter skipping is defined for the embedding adapter only")
+        if len(keep) != L:
+            raise ValueError("keep needs one flag per layer")
+        kept = [l for l in range(L) if keep[l]]
     if recurrent:
         Z = None
         M = memory_recurrent(E, Dw, Uw, act_kind)
+    elif kept:
+        Z = down(E, Dw[kept], act_kind)
+        M = memory(E, Z, Uw[kept])
     else:
-        Z = down(E, Dw, act_kind)
-        M = memory(E, Z, Uw)
-    Kv, Vv = visual_kv(M, gamma, Wk, Wv, B, Nv, Hkv, hd, eps)
-    O = np.stack([text_visual_attention(Q[l], Kv[l], Vv[l], Kt[l], Vt[l], q_pos0, scale)
-                  for l in range(Kv.shape[0])])
+        Z = np.empty((0, E.shape[0], Dw.shape[1]))
+        M = np.empty((0,) + E.shape)
+    if kept:
+        Kv, Vv = visual_kv(M, gamma[kept], Wk[kept], Wv[kept], B, Nv, Hkv, hd, eps)
+    else:
+        Kv = Vv = np.empty((0, B, Hkv, Nv, hd))
+    slot = {l: j for j, l in enumerate(kept)}
+    none = np.empty((B, Hkv, 0, hd))
+    O = np.stack([text_visual_attention(Q[l], Kv[slot[l]] if l in slot else none,
+                                        Vv[slot[l]] if l in slot else none, Kt[l], Vt[l], q_pos0,
+                                        scale)
+                  for l in range(L)])
     return Z, Kv, Vv, O

@@ -33,6 +33,8 @@ EXPORTS = (
     "dv_time_kernel",
     "dv_recurrent_visual_kv_workspace",
     "dv_recurrent_visual_kv",
+    "dv_kept_visual_kv_workspace",
+    "dv_kept_visual_kv",
 )
 
 KERNEL_DOWN, KERNEL_UP, KERNEL_KV, KERNEL_ATTENTION = 0, 1, 2, 3
@@ -82,6 +84,10 @@ def load() -> ctypes.CDLL:
         lib.dv_recurrent_visual_kv_workspace.restype = sz
         lib.dv_recurrent_visual_kv.argtypes = [vp] * 8 + [i32] * 8 + [f32, i32, vp, sz, vp]
         lib.dv_recurrent_visual_kv.restype = i32
+        lib.dv_kept_visual_kv_workspace.argtypes = [ctypes.c_int64, i32, i32, i32, i32]
+        lib.dv_kept_visual_kv_workspace.restype = sz
+        lib.dv_kept_visual_kv.argtypes = [vp] * 9 + [i32] * 8 + [f32, i32, vp, sz, vp]
+        lib.dv_kept_visual_kv.restype = i32
         _lib = lib
         return lib
 
@@ -193,6 +199,42 @@ def recurrent_visual_kv(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, act: int =
     return Kv, Vv
 
 
+def kept_visual_kv_workspace(T: int, d: int, r: int, nkeep: int, dtype: torch.dtype) -> int:
+    code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
+    return int(load().dv_kept_visual_kv_workspace(T, d, r, nkeep, code))
+
+
+def kept_visual_kv(E, Dw, Uw, gamma, Wk, Wv, keep, Kv, Vv, eps: float, act: int = ACT_SILU,
+                   ws: Optional[torch.Tensor] = None, stream=None):
+    """Adapters and K/V only for the layers with keep[l] true; Kv, Vv [nkeep,B,Hkv,Nv,hd]
+    hold the kept layers in order (layer-wise adapter skipping)."""
+    L, r, d = Dw.shape
+    flags = bytes(1 if k else 0 for k in keep)
+    if len(flags) != L:
+        raise ValueError(f"keep has {len(flags)} entries for {L} layers")
+    nkeep = sum(flags)
+    T = E.shape[0]
+    if nkeep == 0:
+        if Kv is not None and Kv.numel() or Vv is not None and Vv.numel():
+            raise ValueError("no layer is kept but Kv/Vv are not empty")
+        return Kv, Vv
+    nk, B, Hkv, Nv, hd = Kv.shape
+    if (nk != nkeep or T != B * Nv or E.shape[1] != d or tuple(Uw.shape) != (L, d, r)
+            or tuple(gamma.shape) != (L, d) or tuple(Wk.shape) != (L, Hkv * hd, d)
+            or Wv.shape != Wk.shape or Vv.shape != Kv.shape):
+        raise ValueError("shape mismatch in kept_visual_kv")
+    code = _dtype_code(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv)
+    if ws is None:
+        ws = torch.empty(kept_visual_kv_workspace(T, d, r, nkeep, E.dtype), dtype=torch.uint8,
+                         device=E.device)
+    keep_arr = (ctypes.c_uint8 * L).from_buffer_copy(flags)
+    _check(load().dv_kept_visual_kv(_ptr(E), _ptr(Dw), _ptr(Uw), _ptr(gamma), _ptr(Wk), _ptr(Wv),
+                                    ctypes.cast(keep_arr, ctypes.c_void_p), _ptr(Kv), _ptr(Vv), B,
+                                    Nv, d, L, r, Hkv, hd, act, float(eps), code, _ptr(ws),
+                                    ws.numel(), _stream(E.device, stream)))
+    return Kv, Vv
+
+
 def text_visual_attention_workspace(B: int, Hq: int, Hkv: int, hd: int, Nv: int, Nq: int,
                                     Nkt: int) -> int:
     return int(load().dv_text_visual_attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nkt))
@@ -203,6 +245,10 @@ def text_visual_attention(Q, Kv, Vv, Kt, Vt, O, q_pos0: int = 0, scale: Optional
     """One layer of Eq. 9. Q, O [B,Nq,Hq,hd]; Kv, Vv [B,Hkv,Nv,hd]; Kt, Vt [B,Hkv,Nkt,hd]."""
     B, Nq, Hq, hd = Q.shape
     _, Hkv, Nkt, _ = Kt.shape
+    if Kv is None or Vv is None:  # a layer without visual keys (skipped adapter)
+        if Kv is not None or Vv is not None:
+            raise ValueError("Kv and Vv must both be given or both be None")
+        Kv = Vv = Q.new_empty((B, Hkv, 0, hd))
     Nv = Kv.shape[2]
     if (tuple(Kv.shape) != (B, Hkv, Nv, hd) or Vv.shape != Kv.shape or Vt.shape != Kt.shape
             or Kt.shape[0] != B or Kt.shape[3] != hd or O.shape != Q.shape):

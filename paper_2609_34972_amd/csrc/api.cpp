@@ -225,6 +225,93 @@ dv_status dv_recurrent_visual_kv(const void* E, const void* Dw, const void* Uw, 
                     "dv_recurrent_visual_kv launch");
 }
 
+// Z of the kept layers (call dtype, 256-byte aligned) followed by the projection slots.
+static size_t kept_z_bytes(int64_t T, int32_t r, int32_t nkeep, int32_t dtype) {
+  return ((size_t)nkeep * (size_t)T * (size_t)r * elem_size(dtype) + 255) / 256 * 256;
+}
+
+size_t dv_kept_visual_kv_workspace(int64_t T, int32_t d, int32_t r, int32_t nkeep,
+                                   int32_t dtype) {
+  if (T <= 0 || d <= 0 || r <= 0 || nkeep <= 0 || (dtype != DV_F32 && dtype != DV_BF16)) return 0;
+  return kept_z_bytes(T, r, nkeep, dtype) + (size_t)nkeep * kv_ws_layer_bytes(T, d, dtype);
+}
+
+dv_status dv_kept_visual_kv(const void* E, const void* Dw, const void* Uw, const void* gamma,
+                            const void* Wk, const void* Wv, const uint8_t* keep, void* Kv,
+                            void* Vv, int32_t B, int32_t Nv, int32_t d, int32_t L, int32_t r,
+                            int32_t Hkv, int32_t hd, int32_t act, float eps, int32_t dtype,
+                            void* ws, size_t ws_bytes, void* stream) {
+  DV_CHECK(check_dtype(dtype));
+  if (B <= 0 || Nv <= 0 || d <= 0 || L <= 0 || r <= 0 || Hkv <= 0 || hd <= 0)
+    return fail(DV_ERR_SHAPE, "sizes must be positive (B=%d Nv=%d d=%d L=%d r=%d Hkv=%d hd=%d)", B,
+                Nv, d, L, r, Hkv, hd);
+  const int64_t T = (int64_t)B * Nv;
+  if (T > kMaxTokens || (int64_t)2 * Hkv * hd > INT32_MAX || L > 65535 ||
+      (int64_t)L * r > INT32_MAX)
+    return fail(DV_ERR_SHAPE, "B*Nv=%lld exceeds %lld (or L > 65535)", (long long)T,
+                (long long)kMaxTokens);
+  if (d % 64 != 0) return fail(DV_ERR_UNSUPPORTED, "d=%d must be a multiple of 64", d);
+  if (r % 16 != 0) return fail(DV_ERR_UNSUPPORTED, "r=%d must be a multiple of 16", r);
+  if (hd != 64 && hd != 128) return fail(DV_ERR_UNSUPPORTED, "hd=%d must be 64 or 128", hd);
+  if (act != DV_ACT_SILU && act != DV_ACT_GELU)
+    return fail(DV_ERR_UNSUPPORTED, "act=%d is not DV_ACT_SILU or DV_ACT_GELU", act);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(DV_ERR_SHAPE, "eps must be finite and >= 0");
+  if (!keep) return fail(DV_ERR_NULL, "keep is NULL");
+  int nkeep = 0;
+  for (int l = 0; l < L; ++l) nkeep += keep[l] != 0;
+  if (nkeep == 0) return ok();
+  DV_CHECK(need_ptr(E, "E"));
+  DV_CHECK(need_ptr(Dw, "Dw"));
+  DV_CHECK(need_ptr(Uw, "Uw"));
+  DV_CHECK(need_ptr(gamma, "gamma"));
+  DV_CHECK(need_ptr(Wk, "Wk"));
+  DV_CHECK(need_ptr(Wv, "Wv"));
+  DV_CHECK(need_ptr(Kv, "Kv"));
+  DV_CHECK(need_ptr(Vv, "Vv"));
+  const size_t zb = kept_z_bytes(T, r, nkeep, dtype);
+  const size_t per_layer = kv_ws_layer_bytes(T, d, dtype);
+  if (!ws || ws_bytes < zb + per_layer)
+    return fail(DV_ERR_WORKSPACE, "workspace of %zu bytes is below the minimum %zu",
+                ws ? ws_bytes : (size_t)0, zb + per_layer);
+  if (!aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
+  const size_t e = elem_size(dtype);
+  const size_t kvw = (size_t)Hkv * hd;
+  const size_t mem_al = ((size_t)T * d * e + 255) / 256 * 256;
+  const int group = (int)std::min<size_t>((size_t)nkeep, (ws_bytes - zb) / per_layer);
+  char* Zall = (char*)ws;
+  char* pw = Zall + zb;
+  const int bf = dtype == DV_BF16 ? 1 : 0;
+  hipStream_t s = (hipStream_t)stream;
+  // Runs of consecutive kept layers [a, b) fill cache slots [c, c + b - a). Weights are
+  // addressed from layer a, Z and the caches from slot c, so each run is an ordinary
+  // all-layer call on shifted base pointers.
+  int c = 0;
+  for (int a = 0; a < L;) {
+    if (!keep[a]) { ++a; continue; }
+    int b = a;
+    while (b < L && keep[b]) ++b;
+    const int n = b - a;
+    char* Z = Zall + (size_t)c * T * r * e;
+    hipError_t err = dv::launch_down_act(E, (const char*)Dw + (size_t)a * r * d * e, Z, T, d, n, r,
+                                         act, bf, s, g_ev);
+    if (err != hipSuccess) return hip_status(err, "dv_kept_visual_kv down launch");
+    for (int g0 = 0; g0 < n; g0 += group) {
+      const int gl = std::min(group, n - g0);
+      const size_t la = (size_t)(a + g0), lc = (size_t)(c + g0);
+      err = dv::launch_project_kv(
+          E, Z + (size_t)g0 * T * r * e, (const char*)Uw + la * d * r * e,
+          (const char*)gamma + la * d * e, (const char*)Wk + la * kvw * d * e,
+          (const char*)Wv + la * kvw * d * e, (char*)Kv + lc * T * kvw * e,
+          (char*)Vv + lc * T * kvw * e, B, Nv, d, r, Hkv, hd, 0, gl, eps, bf, pw,
+          (float*)(pw + (size_t)gl * mem_al), s, g_ev, g0 == 0, g0 + gl >= n);
+      if (err != hipSuccess) return hip_status(err, "dv_kept_visual_kv projection launch");
+    }
+    c += n;
+    a = b;
+  }
+  return ok();
+}
+
 size_t dv_text_visual_attention_workspace(int32_t B, int32_t Hq, int32_t Hkv, int32_t hd,
                                           int32_t Nv, int32_t Nq, int32_t Nkt) {
   if (B <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || (hd != 64 && hd != 128) || Nv < 0 ||

@@ -162,3 +162,40 @@ def test_recurrent_workspace_grows_with_layers(lib):
     a = lib.dv_recurrent_visual_kv_workspace(2304, 4096, 8, 256, BF16)
     b = lib.dv_recurrent_visual_kv_workspace(2304, 4096, 32, 256, BF16)
     assert 0 < a < b and lib.dv_recurrent_visual_kv_workspace(0, 4096, 8, 256, BF16) == 0
+
+
+def kept_call(lib, keep=(1, 0, 1, 1), ws=FAKE, ws_bytes=None, **over):
+    a = dict(E=FAKE, Dw=FAKE, Uw=FAKE, g=FAKE, Wk=FAKE, Wv=FAKE, Kv=FAKE, Vv=FAKE, B=1, Nv=64,
+             d=256, L=4, r=16, Hkv=4, hd=64, act=0, eps=1e-5, dt=F32)
+    a.update(over)
+    karr = None if keep is None else (ctypes.c_uint8 * len(keep))(*keep)
+    if ws_bytes is None:
+        ws_bytes = lib.dv_kept_visual_kv_workspace(a["B"] * a["Nv"], a["d"], a["r"],
+                                                   max(1, sum(keep or ())), a["dt"])
+    return lib.dv_kept_visual_kv(a["E"], a["Dw"], a["Uw"], a["g"], a["Wk"], a["Wv"],
+                                 ctypes.cast(karr, ctypes.c_void_p) if karr else None, a["Kv"],
+                                 a["Vv"], a["B"], a["Nv"], a["d"], a["L"], a["r"], a["Hkv"], a["hd"],
+                                 a["act"], a["eps"], a["dt"], ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(keep=None), NULL), (dict(E=None), NULL), (dict(Kv=None), NULL), (dict(Wk=FAKE + 2), ALIGN),
+    (dict(B=0), SHAPE), (dict(L=0), SHAPE), (dict(eps=float("inf")), SHAPE),
+    (dict(hd=48), UNSUP), (dict(d=96), UNSUP), (dict(r=20), UNSUP), (dict(act=5), UNSUP),
+    (dict(dt=7), UNSUP), (dict(ws=None), WS), (dict(ws_bytes=4096), WS), (dict(ws=FAKE + 8), ALIGN),
+])
+def test_kept_visual_kv_rejects(lib, kw, code):
+    assert kept_call(lib, **kw) == code
+
+
+def test_kept_visual_kv_nothing_kept_is_a_no_op(lib):
+    # Every layer skipped: valid, launches nothing, needs no caches and no workspace.
+    assert kept_call(lib, keep=(0, 0, 0, 0), Kv=None, Vv=None, ws=None, ws_bytes=0) == OK
+
+
+def test_kept_workspace_rules(lib):
+    one = lib.dv_kept_visual_kv_workspace(2304, 4096, 256, 1, BF16)
+    many = lib.dv_kept_visual_kv_workspace(2304, 4096, 256, 17, BF16)
+    proj = lib.dv_project_visual_kv_workspace(2304, 4096, 1, BF16)
+    assert one == proj + 2304 * 256 * 2 and many == 17 * one
+    assert lib.dv_kept_visual_kv_workspace(2304, 4096, 256, 0, BF16) == 0

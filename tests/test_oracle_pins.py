@@ -308,3 +308,35 @@ def test_tiny_workload_pipeline_against_torch():
         np.testing.assert_allclose(Vv[l], v.numpy(), rtol=1e-11, atol=1e-12)
         ref = sdpa_reference(tx["Q"][l], k.numpy(), v.numpy(), tx["Kt"][l], tx["Vt"][l], 0)
         np.testing.assert_allclose(O[l], ref, rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("keep", [(1, 0, 1, 1), (0, 0, 0, 0), (1, 1, 1, 1)], ids=["mixed", "none", "all"])
+def test_layer_skipping_against_torch(keep):
+    """Adapter skipping (appendix on skipping): kept layers follow Eq. 5/7/9 unchanged; a
+    skipped layer has no visual keys and reduces to causal text attention (Eq. 18)."""
+    w = configs.TINY
+    E = synth.as_f64(synth.make_E(w))
+    wt = {k: synth.as_f64(v) for k, v in synth.make_build_weights(w).items()}
+    tx = {k: synth.as_f64(v) for k, v in synth.make_text(w).items()}
+    Z, Kv, Vv, O = oracle.pipeline(E, wt["Dw"], wt["Uw"], wt["gamma"], wt["Wk"], wt["Wv"], tx["Q"],
+                                   tx["Kt"], tx["Vt"], w.B, w.Nv, w.Hkv, w.hd, w.eps, w.act,
+                                   keep=keep)
+    kept = [l for l in range(w.L) if keep[l]]
+    assert Kv.shape[0] == Vv.shape[0] == Z.shape[0] == len(kept) and O.shape[0] == w.L
+    for j, l in enumerate(kept):
+        z = F.gelu(F.linear(t64(E), t64(wt["Dw"][l])))
+        n = F.rms_norm(t64(E) + F.linear(z, t64(wt["Uw"][l])), (w.d,), t64(wt["gamma"][l]), eps=w.eps)
+        k = F.linear(n, t64(wt["Wk"][l])).reshape(w.B, w.Nv, w.Hkv, w.hd).permute(0, 2, 1, 3)
+        np.testing.assert_allclose(Z[j], z.numpy(), rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(Kv[j], k.numpy(), rtol=1e-11, atol=1e-12)
+    for l in range(w.L):
+        if keep[l]:
+            continue
+        ref = F.scaled_dot_product_attention(t64(tx["Q"][l]).transpose(1, 2), t64(tx["Kt"][l]),
+                                             t64(tx["Vt"][l]), is_causal=True)
+        np.testing.assert_allclose(O[l], ref.transpose(1, 2).numpy(), rtol=1e-12, atol=1e-13)
+    if all(keep):
+        _, Kf, _, Of = oracle.pipeline(E, wt["Dw"], wt["Uw"], wt["gamma"], wt["Wk"], wt["Wv"],
+                                       tx["Q"], tx["Kt"], tx["Vt"], w.B, w.Nv, w.Hkv, w.hd, w.eps,
+                                       w.act)
+        assert np.array_equal(Kf, Kv) and np.array_equal(Of, O)
