@@ -77,6 +77,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the decode-shape measurement appended to prefill workloads")
+    p.add_argument("--no-cold", action="store_true",
+                   help="skip the cold-cache steps (512 MiB rewritten before each)")
+    p.add_argument("--no-variants", action="store_true",
+                   help="skip the recurrent-adapter and layer-skipping measurements")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain 1 GiB device copy, whose memory counters calibrate the "
                         "FETCH_SIZE / WRITE_SIZE readings of the kernels")
@@ -114,6 +118,33 @@ def stored_traffic():
         return float(kv["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def percentiles(xs):
+    import numpy as np
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
+            "p90": float(np.percentile(a, 90))}
+
+
+def time_calls(fn, steps, warmup, flush=None):
+    """Per-call times (ms) of fn() from torch events on the current stream. With flush, a
+    buffer larger than the last-level cache is rewritten before every call, outside the
+    timed events (cold runs)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    pairs = [(mk(), mk()) for _ in range(steps)]
+    for a, b in pairs:
+        if flush is not None:
+            flush.add_(1)
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in pairs]
 
 
 def cpu_baseline(w, E, wts, tx, vcache):
@@ -208,13 +239,17 @@ def run_prefill(args, w):
             "attn": [hev.pair() for _ in range(w.L)]} for _ in range(args.steps)]
     mk = lambda: torch.cuda.Event(enable_timing=True)
     t_begin, t_end = mk(), mk()
+    marks = [mk() for _ in range(args.steps + 1)]
     log(f"[bench] timing {args.steps} steps")
     torch.cuda.synchronize()
     t_begin.record()
     for s in range(args.steps):
+        marks[s].record()
         step(evs[s])
+    marks[-1].record()
     t_end.record()
     torch.cuda.synchronize()
+    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
     for k in (dvl.KERNEL_DOWN, dvl.KERNEL_UP, dvl.KERNEL_KV, dvl.KERNEL_ATTENTION):
         dvl.time_kernel(k)
     ms_total = t_begin.elapsed_time(t_end)
@@ -268,6 +303,14 @@ def run_prefill(args, w):
             "step_mfma_frac": (f_build + f_attn) / (ms_step * 1e-3) / 1e12 / peak,
         },
     }
+    out["step_ms_warm"] = percentiles(step_ms)
+    if not args.no_cold:
+        log("[bench] cold steps (512 MiB rewritten between steps)")
+        flush = torch.empty(128 << 20, dtype=torch.float32, device=dev)
+        out["step_ms_cold"] = percentiles(time_calls(step, max(3, args.steps // 4), 1, flush))
+        del flush
+    if not args.no_variants:
+        out["variants"] = run_variants(args, w, Eg, wg, tg, peak, f_build, ms_step)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle baseline")
         vc = synth.make_visual_cache(w, layers=[0])
@@ -275,6 +318,66 @@ def run_prefill(args, w):
     del Eg, wg, tg, Z, Kv, Vv, O, ws_kv, ws_at
     torch.cuda.empty_cache()
     return out
+
+
+def run_variants(args, w, Eg, wg, tg, peak, f_build, ms_full_step):
+    """The recurrent adapter (Eq. 6) and layer-wise adapter skipping on the same inputs."""
+    import torch
+
+    import paper_2609_34972_amd as dvl
+    from paper_2609_34972_amd import configs
+
+    dev = Eg.device
+    dt = Eg.dtype
+    res = {}
+    steps, warm = max(5, args.steps // 2), 2
+    # recurrent adapter: per-layer chain, then the K/V projection of every layer
+    log("[bench] variant: recurrent adapter")
+    Kv = torch.empty(w.L, w.B, w.Hkv, w.Nv, w.hd, dtype=dt, device=dev)
+    Vv = torch.empty_like(Kv)
+    ws = torch.empty(dvl.recurrent_visual_kv_workspace(w.T, w.d, w.L, w.r, dt), dtype=torch.uint8,
+                     device=dev)
+    t = percentiles(time_calls(lambda: dvl.recurrent_visual_kv(
+        Eg, wg["Dw"], wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv, Vv, eps=w.eps, act=w.act,
+        ws=ws), steps, warm))
+    res["recurrent_build_kv"] = {
+        "ms": t, "visual_tokens_per_s": w.T / (t["median"] * 1e-3),
+        "tflops": f_build / (t["median"] * 1e-3) / 1e12,
+        "mfma_frac": f_build / (t["median"] * 1e-3) / 1e12 / peak}
+    del Kv, Vv, ws
+    # adapter skipping as in the appendix tables: first 5 and last 10 layers skipped
+    if w.L > 15:
+        keep = [0] * 5 + [1] * (w.L - 15) + [0] * 10
+        nk = sum(keep)
+        log(f"[bench] variant: adapters of the first 5 and last 10 layers skipped ({nk} kept)")
+        Kv = torch.empty(nk, w.B, w.Hkv, w.Nv, w.hd, dtype=dt, device=dev)
+        Vv = torch.empty_like(Kv)
+        ws = torch.empty(dvl.kept_visual_kv_workspace(w.T, w.d, w.r, nk, dt), dtype=torch.uint8,
+                         device=dev)
+        O = torch.empty_like(tg["Q"])
+        na = dvl.text_visual_attention_workspace(w.B, w.Hq, w.Hkv, w.hd, w.Nv, w.Nq, w.Nkt)
+        wsa = torch.empty(max(na, 16), dtype=torch.uint8, device=dev)
+        slot = {l: j for j, l in enumerate(l for l in range(w.L) if keep[l])}
+
+        def kept_step():
+            dvl.kept_visual_kv(Eg, wg["Dw"], wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], keep, Kv,
+                               Vv, eps=w.eps, act=w.act, ws=ws)
+            for l in range(w.L):
+                j = slot.get(l)
+                dvl.text_visual_attention(tg["Q"][l], Kv[j] if j is not None else None,
+                                          Vv[j] if j is not None else None, tg["Kt"][l],
+                                          tg["Vt"][l], O[l], q_pos0=w.q_pos0, ws=wsa)
+
+        t = percentiles(time_calls(kept_step, steps, warm))
+        res["skip_first5_last10"] = {
+            "kept_layers": nk, "ms_per_step": t,
+            "visual_tokens_per_s": w.T / (t["median"] * 1e-3),
+            "speedup_vs_all_layers": ms_full_step / t["median"],
+            "visual_cache_bytes": 2 * Kv.numel() * Kv.element_size(),
+            "visual_cache_bytes_all_layers": 2 * w.L * w.T * w.kv * Kv.element_size()}
+        del Kv, Vv, ws, O, wsa
+    torch.cuda.empty_cache()
+    return res
 
 
 def run_decode(args, w, layers_timed=None):
