@@ -277,6 +277,12 @@ __global__ __launch_bounds__(DownP::NT) void k_down_act_p(const bf16* __restrict
   }
 }
 
+// Up-projection epilogue staging: the fp32 tile, rows padded by 4 floats so the transposed
+// accumulator writes (32 rows at one column per instruction) hit distinct banks.
+constexpr int kUpPitch = UpP::BN + 4;
+constexpr int kUpLdsBytes = UpP::BM * kUpPitch * 4 > UpP::LDS_BYTES ? UpP::BM * kUpPitch * 4
+                                                                     : UpP::LDS_BYTES;
+
 __global__ __launch_bounds__(UpP::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        const bf16* __restrict__ Z,
                                                        const bf16* __restrict__ Uw,
@@ -295,51 +301,69 @@ __global__ __launch_bounds__(UpP::NT) void k_up_norm_p(const bf16* __restrict__ 
                1 << 30, ldb};
   BufOperand B{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
                1 << 30, ldb};
+  // The epilogue's rows of E (16 lanes x 16 bytes per 128-column row, BM/16 rows per thread)
+  // are fetched before the main loop so they arrive while the MFMAs run.
+  constexpr int kRows = C::BM / (C::NT / 16);
+  const int c8 = (threadIdx.x & 15) * 8;
+  const int r16 = threadIdx.x >> 4;
+  const bool col_ok = n0 + c8 < d;  // d is a multiple of 64, so a chunk is all in or all out
+  u32x4 e_pre[kRows];
+#pragma unroll
+  for (int i = 0; i < kRows; ++i) {
+    const int row = m0 + r16 + i * (C::NT / 16);
+    e_pre[i] = (row < T && col_ok) ? *(const u32x4*)(E + (int64_t)row * d + n0 + c8) : u32x4{};
+  }
   f32x16 acc[C::FM][C::FN];
   pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
 
+  // 1. Z_l U_l tile (fp32) into LDS. The main loop's last LDS read precedes its last barrier.
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
-  const bf16* gl = gamma + (int64_t)l * d;
-  bf16* Ml = Mg + (int64_t)lz * T * d;
-  float* red = (float*)smem;  // [WGN][BM]; the main loop ended with a barrier
+  float* tile = (float*)smem;
 #pragma unroll
   for (int a = 0; a < C::FM; ++a) {
     const int rl = wm * C::WM + a * 32 + (lane & 31);
-    const int row = m0 + rl;
-    const bool ok = row < T;
-    float ss = 0.f;
 #pragma unroll
     for (int b = 0; b < C::FN; ++b)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
-        if (!ok || n >= d) continue;
-        float e[4], g[4];
-        load4_bf16(E + (int64_t)row * d + n, e);
-        load4_bf16(gl + n, g);
-        float m[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          m[u] = acc[a][b][4 * q + u] + e[u];
-          ss += m[u] * m[u];
-        }
-        store4_bf16(Ml + (int64_t)row * d + n, m[0] * g[0], m[1] * g[1], m[2] * g[2], m[3] * g[3],
-                    [](float x) { return x; });
+        const int c = wn * C::WN + b * 32 + pipe_col(lane, q);
+        const f32x16& v = acc[a][b];
+        *(f32x4*)(tile + rl * kUpPitch + c) = f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
       }
-    ss += shfl_xor(ss, 32);  // the two lane halves hold the same row
-    if (lane < 32) red[wn * C::BM + rl] = ss;
   }
   __syncthreads();
+  // 2. Rows of the tile: 16 lanes x 8 columns each cover the 128 columns, so E, gamma and the
+  //    output move as whole 16-byte pieces of a row, and the row's sum of squares over this
+  //    column tile is a 16-lane shuffle.
+  const bf16* gl = gamma + (int64_t)l * d;
+  bf16* Ml = Mg + (int64_t)lz * T * d;
   const int np = (d + C::BN - 1) / C::BN;
-  for (int rr = threadIdx.x; rr < C::BM; rr += C::NT) {
-    const int row = m0 + rr;
-    if (row < T) {
-      float s = 0.f;
+  bf16x8 g8 = {};
+  if (col_ok) g8 = __builtin_bit_cast(bf16x8, *(const u32x4*)(gl + n0 + c8));
 #pragma unroll
-      for (int w = 0; w < C::WGN; ++w) s += red[w * C::BM + rr];
-      ssq[((int64_t)lz * np + blockIdx.x) * T + row] = s;
+  for (int i = 0; i < kRows; ++i) {
+    const int rr = r16 + i * (C::NT / 16);
+    const int row = m0 + rr;
+    float ss = 0.f;
+    if (row < T && col_ok) {
+      const bf16x8 e8 = __builtin_bit_cast(bf16x8, e_pre[i]);
+      const f32x4 p0 = *(const f32x4*)(tile + rr * kUpPitch + c8);
+      const f32x4 p1 = *(const f32x4*)(tile + rr * kUpPitch + c8 + 4);
+      bf16x8 o;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float m = (u < 4 ? p0[u] : p1[u - 4]) + (float)e8[u];
+        ss += m * m;
+        o[u] = (bf16)(m * (float)g8[u]);
+      }
+      *(u32x4*)(Ml + (int64_t)row * d + n0 + c8) = __builtin_bit_cast(u32x4, o);
     }
+    ss += shfl_xor(ss, 1);
+    ss += shfl_xor(ss, 2);
+    ss += shfl_xor(ss, 4);
+    ss += shfl_xor(ss, 8);
+    if ((threadIdx.x & 15) == 0 && row < T) ssq[((int64_t)lz * np + blockIdx.x) * T + row] = ss;
   }
 }
 
@@ -512,6 +536,7 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
   static_assert(KvP::NT == 2 * KvP::BM, "two threads per row finish the row scales");
   static bool once = [] {
     allow_lds(k_kv_proj_p, kv_lds);
+    allow_lds(k_up_norm_p, kUpLdsBytes);
     return true;
   }();
   (void)once;
@@ -519,7 +544,7 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
   const int np = cdiv(d, UpP::BN);
   dim3 gu(np, cdiv(T_, UpP::BM), nl);
   if (first) record(ev.up[0], s);
-  k_up_norm_p<<<gu, dim3(UpP::NT), UpP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Z,
+  k_up_norm_p<<<gu, dim3(UpP::NT), kUpLdsBytes, s>>>((const bf16*)E, (const bf16*)Z,
                                                          (const bf16*)Uw, (const bf16*)gamma,
                                                          (bf16*)Mg, ssq, T_, d, r, l0);
   if (last) record(ev.up[1], s);
