@@ -56,6 +56,8 @@ def _load():
         lib.dvref_visual_kv.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, f64, P, P]
         lib.dvref_text_visual_attention.argtypes = [P, P, P, P, P, P] + [i32] * 8 + [f64]
         lib.dvref_text_visual_attention.restype = i32
+        lib.dvref_kv_epilogue.argtypes = [P, P] + [i32] * 5 + [P, P, P, f64, ctypes.c_void_p] + [i32] * 3 + [f64]
+        lib.dvref_kv_epilogue.restype = i32
         lib.dvref_attention_weights.argtypes = [P, P, P, P] + [i32] * 8 + [f64, i32, i32, i32]
         lib.dvref_attention_weights.restype = i32
         _lib = lib
@@ -166,6 +168,30 @@ def attention_weights(Q, Kv, Kt, q_pos0: int, b: int, i: int, h: int,
     if n < 0:
         raise ValueError("invalid attention shape")
     return p[:n].copy()
+
+
+def kv_epilogue(Kv, Vv, k_bias=None, v_bias=None, k_norm=None, kn_eps: float = 1e-6, pos=None,
+                sections=None, theta: float = 10000.0):
+    """Backbone epilogue on visual K/V [L,B,Hkv,Nv,hd]: projection bias, per-head key RMSNorm
+    and rotary embedding at the tokens' positions pos [B,3,Nv] with multimodal sections (the
+    paper keeps visual positions unchanged, so the backbone's key treatment applies to them).
+    Returns new arrays; None skips a step."""
+    Kv, Vv = _c(Kv).copy(), _c(Vv).copy()
+    L, B, Hkv, Nv, hd = Kv.shape
+    sections = (hd // 2, 0, 0) if sections is None else tuple(int(x) for x in sections)
+    posa = None
+    if pos is not None:
+        posa = np.ascontiguousarray(pos, dtype=np.int32)
+        if posa.shape != (B, 3, Nv):
+            raise ValueError("pos must be [B, 3, Nv]")
+    extra = [None if a is None else _c(a) for a in (k_bias, v_bias, k_norm)]
+    rc = _load().dvref_kv_epilogue(_p(Kv), _p(Vv), L, B, Hkv, Nv, hd,
+                                   *[None if a is None else _p(a) for a in extra], float(kn_eps),
+                                   None if posa is None else posa.ctypes.data, *sections,
+                                   float(theta))
+    if rc != 0:
+        raise ValueError("rotary sections must add up to hd/2")
+    return Kv, Vv
 
 
 def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, B: int, Nv: int, Hkv: int, hd: int, eps: float):

@@ -25,7 +25,9 @@
  *   - the softmax scale is an argument (1/sqrt(hd) by default, as in the
  *     read-out of Appendix K);
  *   - query head h reads key/value head h / (Hq/Hkv);
- *   - no positional rotation is applied to visual keys (Eq. 7 has none).
+ *   - no positional rotation is applied to visual keys by Eq. 7 itself; the
+ *     backbone epilogue (bias, per-head key norm, rotary embedding at the
+ *     visual tokens' unchanged positions) is a separate, optional step.
  *
  * Sums run sequentially in fp64. OpenMP only distributes independent output
  * elements over threads; it changes no arithmetic.
@@ -147,6 +149,59 @@ void dvref_visual_kv(const double* M, const double* gamma, const double* Wk, con
       free(nrm);
     }
   }
+}
+
+/* Backbone epilogue of the visual keys and values (outside Eq. 7). The paper keeps every
+ * visual token at its original position, so a backbone whose attention adds a projection
+ * bias, normalises each key head or rotates keys by position does the same to the
+ * reconstructed visual K/V. In the backbone's order, per layer l, token (b, i), head h:
+ *   K += k_bias[l], V += v_bias[l]                              (projection bias)
+ *   K_h <- K_h * (mean_c K_h[c]^2 + kn_eps)^-1/2 * k_norm[l]    (per-head key RMSNorm)
+ *   rotary embedding of K_h: channel j < hd/2 pairs with channel j + hd/2 and turns by the
+ *   angle p * theta^(-2j/hd), where p = pos[b][a][i] and the position axis a is 0 for
+ *   j < sec0, 1 for j < sec0 + sec1 and 2 otherwise (sections of a multimodal rotary
+ *   embedding; sec0 = hd/2 is the one-dimensional case):
+ *      (k_j, k_{j+hd/2}) <- (k_j cos - k_{j+hd/2} sin,  k_{j+hd/2} cos + k_j sin).
+ * NULL k_bias / v_bias / k_norm / pos skips that step. In place on Kv, Vv [L,B,Hkv,Nv,hd];
+ * k_bias, v_bias [L, Hkv*hd]; k_norm [L, hd]; pos [B, 3, Nv]. Returns -1 if the sections do
+ * not add up to hd/2 (or hd is odd), else 0. */
+int dvref_kv_epilogue(double* Kv, double* Vv, int L, int B, int Hkv, int Nv, int hd,
+                      const double* k_bias, const double* v_bias, const double* k_norm,
+                      double kn_eps, const int* pos, int sec0, int sec1, int sec2, double theta) {
+  const int half = hd / 2;
+  if (hd % 2 != 0 || sec0 < 0 || sec1 < 0 || sec2 < 0 || sec0 + sec1 + sec2 != half) return -1;
+  const int64_t rows = (int64_t)L * B * Hkv * Nv;
+#pragma omp parallel for schedule(static)
+  for (int64_t row = 0; row < rows; ++row) {
+    const int i = (int)(row % Nv);
+    const int h = (int)((row / Nv) % Hkv);
+    const int b = (int)((row / ((int64_t)Nv * Hkv)) % B);
+    const int l = (int)(row / ((int64_t)Nv * Hkv * B));
+    double* k = Kv + row * hd;
+    double* v = Vv + row * hd;
+    if (k_bias)
+      for (int c = 0; c < hd; ++c) k[c] += k_bias[(int64_t)l * Hkv * hd + h * hd + c];
+    if (v_bias)
+      for (int c = 0; c < hd; ++c) v[c] += v_bias[(int64_t)l * Hkv * hd + h * hd + c];
+    if (k_norm) {
+      double ss = 0.0;
+      for (int c = 0; c < hd; ++c) ss += k[c] * k[c];
+      const double rho = 1.0 / sqrt(ss / (double)hd + kn_eps);
+      for (int c = 0; c < hd; ++c) k[c] = k[c] * rho * k_norm[(int64_t)l * hd + c];
+    }
+    if (pos) {
+      for (int j = 0; j < half; ++j) {
+        const int a = j < sec0 ? 0 : (j < sec0 + sec1 ? 1 : 2);
+        const double p = (double)pos[((int64_t)b * 3 + a) * Nv + i];
+        const double ang = p * pow(theta, -2.0 * (double)j / (double)hd);
+        const double cs = cos(ang), sn = sin(ang);
+        const double x1 = k[j], x2 = k[j + half];
+        k[j] = x1 * cs - x2 * sn;
+        k[j + half] = x2 * cs + x1 * sn;
+      }
+    }
+  }
+  return 0;
 }
 
 /* Eq. 9 for one layer. Query (b, i, h) reads key/value head g = h / (Hq/Hkv) and the key set

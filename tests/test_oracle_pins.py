@@ -340,3 +340,103 @@ def test_layer_skipping_against_torch(keep):
                                        tx["Q"], tx["Kt"], tx["Vt"], w.B, w.Nv, w.Hkv, w.hd, w.eps,
                                        w.act)
         assert np.array_equal(Kf, Kv) and np.array_equal(Of, O)
+
+
+# ---- backbone epilogue of the visual keys (bias, per-head key norm, rotary embedding) ----
+
+def _rope_complex(x, pos, sections, theta):
+    """Rotary embedding as complex multiplication: channel pair (j, j + hd/2) is the complex
+    number x_j + i x_{j+hd/2}, turned by exp(i p theta^(-2j/hd)) (numpy complex arithmetic)."""
+    L, B, H, N, hd = x.shape
+    half = hd // 2
+    axis = np.repeat(np.arange(3), sections)                      # position axis of each j
+    p = np.asarray(pos, dtype=np.float64)[:, axis, :]              # [B, half, N]
+    freq = theta ** (-2.0 * np.arange(half) / hd)                  # [half]
+    rot = np.exp(1j * p * freq[None, :, None])                     # [B, half, N]
+    z = (x[..., :half] + 1j * x[..., half:]) * rot.transpose(0, 2, 1)[None, :, None]
+    return np.concatenate([z.real, z.imag], axis=-1)
+
+
+def _pos(B, N, seed, spread=5000):
+    return np.random.default_rng(seed).integers(0, spread, size=(B, 3, N)).astype(np.int32)
+
+
+@pytest.mark.parametrize("hd,sections", [(64, (32, 0, 0)), (128, (16, 24, 24)), (128, (0, 40, 24))])
+def test_rope_is_complex_rotation(hd, sections):
+    K, V = rnd(61, 2, 2, 3, 7, hd), rnd(62, 2, 2, 3, 7, hd)
+    pos = _pos(2, 7, 63)
+    Kr, Vr = oracle.kv_epilogue(K, V, pos=pos, sections=sections, theta=1e6)
+    np.testing.assert_allclose(Kr, _rope_complex(K, pos, sections, 1e6), rtol=1e-12, atol=1e-12)
+    assert np.array_equal(Vr, V)  # values are never rotated
+
+
+def test_rope_preserves_pair_norms_and_is_identity_at_zero():
+    K = rnd(64, 1, 1, 2, 9, 128)
+    Kr, _ = oracle.kv_epilogue(K, K, pos=_pos(1, 9, 65))
+    n = lambda x: x[..., :64] ** 2 + x[..., 64:] ** 2
+    np.testing.assert_allclose(n(Kr), n(K), rtol=1e-12)
+    K0, _ = oracle.kv_epilogue(K, K, pos=np.zeros((1, 3, 9), np.int32))
+    assert np.array_equal(K0, K)
+
+
+def test_rope_scores_depend_only_on_position_difference():
+    # <R(p) q, R(p') k> = <R(p + s) q, R(p' + s) k>: the relative-position property.
+    hd = 128
+    q, k = rnd(66, 1, 1, 1, 1, hd), rnd(67, 1, 1, 1, 1, hd)
+    def score(pq, pk):
+        rq, _ = oracle.kv_epilogue(q, q, pos=np.full((1, 3, 1), pq, np.int32))
+        rk, _ = oracle.kv_epilogue(k, k, pos=np.full((1, 3, 1), pk, np.int32))
+        return float((rq * rk).sum())
+    assert score(10, 3) == pytest.approx(score(1010, 1003), rel=1e-10)
+    assert score(10, 3) != pytest.approx(score(10, 4), rel=1e-6)
+
+
+def test_multimodal_rope_with_equal_axes_is_1d_rope():
+    K = rnd(68, 2, 1, 2, 5, 128)
+    p1 = _pos(1, 5, 69)[:, :1, :]
+    pos = np.repeat(p1, 3, axis=1)
+    a, _ = oracle.kv_epilogue(K, K, pos=pos, sections=(16, 24, 24))
+    b, _ = oracle.kv_epilogue(K, K, pos=pos, sections=(64, 0, 0))
+    np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-14)
+
+
+def test_key_norm_matches_torch_and_bias_is_additive():
+    L, B, H, N, hd = 2, 2, 3, 4, 64
+    K, V = rnd(70, L, B, H, N, hd), rnd(71, L, B, H, N, hd)
+    kb, vb, kn = rnd(72, L, H * hd), rnd(73, L, H * hd), 1 + 0.1 * rnd(74, L, hd)
+    Kb, Vb = oracle.kv_epilogue(K, V, k_bias=kb, v_bias=vb)
+    np.testing.assert_allclose(Kb - K, np.broadcast_to(kb.reshape(L, 1, H, 1, hd), K.shape), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(Vb - V, np.broadcast_to(vb.reshape(L, 1, H, 1, hd), V.shape), rtol=1e-12, atol=1e-13)
+    Kn, Vn = oracle.kv_epilogue(K, V, k_norm=kn, kn_eps=1e-6)
+    for l in range(L):
+        ref = F.rms_norm(t64(K[l]), (hd,), t64(kn[l]), eps=1e-6).numpy()
+        np.testing.assert_allclose(Kn[l], ref, rtol=1e-12, atol=1e-13)
+    assert np.array_equal(Vn, V)
+
+
+def test_epilogue_order_bias_then_norm_then_rope():
+    L, B, H, N, hd = 1, 1, 2, 3, 128
+    K, V = rnd(75, L, B, H, N, hd), rnd(76, L, B, H, N, hd)
+    kb, kn, pos = rnd(77, L, H * hd), 1 + 0.1 * rnd(78, L, hd), _pos(B, N, 79)
+    full, _ = oracle.kv_epilogue(K, V, k_bias=kb, k_norm=kn, pos=pos, sections=(16, 24, 24))
+    step, _ = oracle.kv_epilogue(K, V, k_bias=kb)
+    step, _ = oracle.kv_epilogue(step, V, k_norm=kn)
+    np.testing.assert_allclose(full, _rope_complex(step, pos, (16, 24, 24), 1e4), rtol=1e-10, atol=1e-11)
+
+
+def test_rotated_visual_keys_shift_invariant_attention():
+    # Rotating visual and text keys and the queries at positions shifted by a common s leaves
+    # Eq. 9's output unchanged (scores depend on position differences only).
+    B, H, Nv, Nt, hd = 1, 2, 6, 4, 64
+    Q, Kv, Vv = rnd(80, B, Nt, H, hd), rnd(81, 1, B, H, Nv, hd), rnd(82, 1, B, H, Nv, hd)
+    Kt, Vt = rnd(83, 1, B, H, Nt, hd), rnd(84, 1, B, H, Nt, hd)
+    def run(s):
+        pv = np.broadcast_to(np.arange(Nv, dtype=np.int32) + s, (B, 3, Nv)).copy()
+        pt = np.broadcast_to(np.arange(Nt, dtype=np.int32) + Nv + s, (B, 3, Nt)).copy()
+        kv, _ = oracle.kv_epilogue(Kv, Vv, pos=pv)
+        kt, _ = oracle.kv_epilogue(Kt, Vt, pos=pt)
+        q = Q.transpose(0, 2, 1, 3)[None]                          # [1,B,H,Nt,hd]
+        qr, _ = oracle.kv_epilogue(q, q, pos=pt)
+        qr = qr[0].transpose(0, 2, 1, 3)
+        return oracle.text_visual_attention(qr, kv[0], Vv[0], kt[0], Vt[0], 0)
+    np.testing.assert_allclose(run(0), run(777), rtol=1e-11, atol=1e-12)
