@@ -111,6 +111,49 @@ dv_status dv_recurrent_visual_kv(const void* E, const void* Dw, const void* Uw, 
                                  size_t ws_bytes, void* stream);
 
 /*
+ * Backbone epilogue of the visual K/V (outside Eq. 7). The paper keeps every visual token at
+ * its original position (appendix on hidden-state compression), so a backbone that adds a
+ * bias to its K/V projections, normalises each key head or rotates keys by position does the
+ * same to the reconstructed visual K/V, in this order, for layer l, token (b, i), head h:
+ *   K += k_bias[l],  V += v_bias[l]
+ *   K_h <- K_h * (mean_c K_h[c]^2 + k_norm_eps)^-1/2 * k_norm[l]      (per-head key RMSNorm)
+ *   rotary embedding of K_h: channel j < hd/2 pairs with channel j + hd/2 and turns by the
+ *   angle p * rope_theta^(-2j/hd), p = positions[b][a][i], where the position axis a is 0
+ *   for j < rope_sections[0], 1 for j < rope_sections[0] + rope_sections[1], 2 otherwise
+ *   (multimodal rotary sections; {hd/2, 0, 0} is the one-dimensional rotation):
+ *       (k_j, k_{j+hd/2}) <- (k_j cos - k_{j+hd/2} sin,  k_{j+hd/2} cos + k_j sin).
+ * A NULL k_bias, v_bias, k_norm or positions skips its step. bf16 runs round the projection
+ * to bf16 once before the key norm and the rotation (with the bias included when r is a
+ * multiple of 64, before it otherwise) and the result once more at the end.
+ */
+typedef struct {
+  const void* k_bias;        /* [L, Hkv*hd] in the call dtype, 16-byte aligned, or NULL */
+  const void* v_bias;        /* [L, Hkv*hd] in the call dtype, 16-byte aligned, or NULL */
+  const void* k_norm;        /* [L, hd] in the call dtype, 16-byte aligned, or NULL */
+  float k_norm_eps;          /* finite, >= 0 */
+  const int32_t* positions;  /* device [B, 3, Nv] position ids per axis, or NULL: no rotation */
+  int32_t rope_sections[3];  /* non-negative, adding up to hd/2 (read only with positions) */
+  float rope_theta;          /* finite, > 0 (read only with positions) */
+} dv_kv_epilogue;
+
+/*
+ * dv_project_visual_kv followed by the backbone epilogue above (fused into the bf16 K/V
+ * kernel). epi may be NULL (then identical to dv_project_visual_kv). ws holds the rotary
+ * table (T * hd * 4 bytes, 256-aligned) followed by the projection workspace: at least
+ * dv_project_visual_kv_ex_workspace(B*Nv, d, 1, hd, dtype) bytes;
+ * dv_project_visual_kv_ex_workspace(B*Nv, d, nl, hd, dtype) bytes project all nl layers in one
+ * launch.
+ */
+size_t dv_project_visual_kv_ex_workspace(int64_t T, int32_t d, int32_t nl, int32_t hd,
+                                         int32_t dtype);
+dv_status dv_project_visual_kv_ex(const void* E, const void* Z, const void* Uw, const void* gamma,
+                                  const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
+                                  int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
+                                  int32_t hd, int32_t l0, int32_t nl, float eps,
+                                  const dv_kv_epilogue* epi, int32_t dtype, void* ws,
+                                  size_t ws_bytes, void* stream);
+
+/*
  * Layer-wise adapter skipping (appendix on adapter skipping, Tables 14 and 15): the
  * embedding adapter (Eq. 4-5) and the K/V projection (Eq. 7) run only for the layers
  * with keep[l] != 0. A skipped layer gets no visual keys at all (its attention runs

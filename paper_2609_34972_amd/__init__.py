@@ -8,15 +8,16 @@ Eq. 9). The arithmetic runs in hand-written HIP kernels behind the C ABI of
 ``include/deltavision.h``; this package only marshals tensors into it.
 """
 from ._lib import (ACT_GELU, ACT_SILU, KERNEL_ATTENTION, KERNEL_DOWN, KERNEL_KV, KERNEL_UP,
-                   DeltaVisionError, build_visual_memory, kept_visual_kv,
-                   kept_visual_kv_workspace, load, project_visual_kv,
+                   DeltaVisionError, KVEpilogue, build_visual_memory, kept_visual_kv,
+                   kept_visual_kv_workspace, load, project_visual_kv, project_visual_kv_ex_workspace,
                    project_visual_kv_workspace, recurrent_visual_kv,
                    recurrent_visual_kv_workspace, text_visual_attention,
                    text_visual_attention_workspace, time_kernel)
 
 __all__ = [
     "ACT_SILU", "ACT_GELU", "DeltaVisionError", "load", "build_visual_memory",
-    "project_visual_kv", "project_visual_kv_workspace", "recurrent_visual_kv",
+    "project_visual_kv", "project_visual_kv_workspace", "project_visual_kv_ex_workspace",
+    "KVEpilogue", "recurrent_visual_kv",
     "recurrent_visual_kv_workspace", "kept_visual_kv", "kept_visual_kv_workspace",
     "text_visual_attention",
     "text_visual_attention_workspace", "time_kernel", "KERNEL_DOWN", "KERNEL_UP", "KERNEL_KV",

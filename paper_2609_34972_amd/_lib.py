@@ -10,7 +10,8 @@ from __future__ import annotations
 import ctypes
 import os
 import threading
-from typing import Optional
+from dataclasses import dataclass
+from typing import Optional, Tuple
 
 import torch
 
@@ -35,7 +36,31 @@ EXPORTS = (
     "dv_recurrent_visual_kv",
     "dv_kept_visual_kv_workspace",
     "dv_kept_visual_kv",
+    "dv_project_visual_kv_ex_workspace",
+    "dv_project_visual_kv_ex",
 )
+
+
+class _KvEpilogue(ctypes.Structure):
+    """Mirror of dv_kv_epilogue."""
+    _fields_ = [("k_bias", ctypes.c_void_p), ("v_bias", ctypes.c_void_p),
+                ("k_norm", ctypes.c_void_p), ("k_norm_eps", ctypes.c_float),
+                ("positions", ctypes.c_void_p), ("rope_sections", ctypes.c_int32 * 3),
+                ("rope_theta", ctypes.c_float)]
+
+
+@dataclass
+class KVEpilogue:
+    """Backbone epilogue of the visual K/V: projection bias [L, Hkv*hd], per-head key RMSNorm
+    weight [L, hd] (call dtype), and rotary embedding at int32 positions [B, 3, Nv] (axes of a
+    multimodal rotary embedding; sections default to (hd/2, 0, 0), the 1-D rotation)."""
+    k_bias: Optional[torch.Tensor] = None
+    v_bias: Optional[torch.Tensor] = None
+    k_norm: Optional[torch.Tensor] = None
+    k_norm_eps: float = 1e-6
+    positions: Optional[torch.Tensor] = None
+    rope_sections: Optional[Tuple[int, int, int]] = None
+    rope_theta: float = 10000.0
 
 KERNEL_DOWN, KERNEL_UP, KERNEL_KV, KERNEL_ATTENTION = 0, 1, 2, 3
 
@@ -68,6 +93,10 @@ def load() -> ctypes.CDLL:
         lib.dv_project_visual_kv_workspace.restype = sz
         lib.dv_project_visual_kv.argtypes = [vp] * 8 + [i32] * 9 + [f32, i32, vp, sz, vp]
         lib.dv_project_visual_kv.restype = i32
+        lib.dv_project_visual_kv_ex_workspace.argtypes = [i64, i32, i32, i32, i32]
+        lib.dv_project_visual_kv_ex_workspace.restype = sz
+        lib.dv_project_visual_kv_ex.argtypes = ([vp] * 8 + [i32] * 9 + [f32, ctypes.POINTER(_KvEpilogue), i32, vp, sz, vp])
+        lib.dv_project_visual_kv_ex.restype = i32
         lib.dv_text_visual_attention_workspace.argtypes = [i32] * 7
         lib.dv_text_visual_attention_workspace.restype = sz
         lib.dv_text_visual_attention.argtypes = [vp] * 6 + [i32] * 8 + [f32, i32, vp, sz, vp]
@@ -150,9 +179,35 @@ def project_visual_kv_workspace(T: int, d: int, nl: int, dtype: torch.dtype) -> 
     return int(load().dv_project_visual_kv_workspace(T, d, nl, code))
 
 
+def project_visual_kv_ex_workspace(T: int, d: int, nl: int, hd: int, dtype: torch.dtype) -> int:
+    code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
+    return int(load().dv_project_visual_kv_ex_workspace(T, d, nl, hd, code))
+
+
+def _epilogue_struct(epi: KVEpilogue, L: int, B: int, Nv: int, Hkv: int, hd: int, dtype):
+    def tensor(t, shape, dt, name):
+        if t is None:
+            return None
+        if tuple(t.shape) != shape or t.dtype != dt or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {dt} tensor of shape {shape}")
+        return t.data_ptr()
+    st = _KvEpilogue()
+    st.k_bias = tensor(epi.k_bias, (L, Hkv * hd), dtype, "k_bias")
+    st.v_bias = tensor(epi.v_bias, (L, Hkv * hd), dtype, "v_bias")
+    st.k_norm = tensor(epi.k_norm, (L, hd), dtype, "k_norm")
+    st.k_norm_eps = float(epi.k_norm_eps)
+    st.positions = tensor(epi.positions, (B, 3, Nv), torch.int32, "positions")
+    sec = epi.rope_sections if epi.rope_sections is not None else (hd // 2, 0, 0)
+    st.rope_sections = (ctypes.c_int32 * 3)(*[int(x) for x in sec])
+    st.rope_theta = float(epi.rope_theta)
+    return st
+
+
 def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, l0: int = 0,
-                      nl: Optional[int] = None, ws: Optional[torch.Tensor] = None, stream=None):
-    """Memories, RMSNorm and visual K/V of layers l0..l0+nl-1 into Kv, Vv [L,B,Hkv,Nv,hd]."""
+                      nl: Optional[int] = None, ws: Optional[torch.Tensor] = None, stream=None,
+                      epilogue: Optional[KVEpilogue] = None):
+    """Memories, RMSNorm and visual K/V of layers l0..l0+nl-1 into Kv, Vv [L,B,Hkv,Nv,hd],
+    optionally followed by the backbone epilogue (bias, key norm, rotary embedding)."""
     L, B, Hkv, Nv, hd = Kv.shape
     T, d = E.shape
     r = Z.shape[2]
@@ -163,12 +218,23 @@ def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, l0: int = 0,
             or Wv.shape != Wk.shape or Vv.shape != Kv.shape):
         raise ValueError("shape mismatch in project_visual_kv")
     code = _dtype_code(E, Z, Uw, gamma, Wk, Wv, Kv, Vv)
+    lib = load()
+    if epilogue is None:
+        if ws is None:
+            ws = torch.empty(project_visual_kv_workspace(T, d, nl, E.dtype), dtype=torch.uint8,
+                             device=E.device)
+        _check(lib.dv_project_visual_kv(_ptr(E), _ptr(Z), _ptr(Uw), _ptr(gamma), _ptr(Wk),
+                                        _ptr(Wv), _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, l0,
+                                        nl, float(eps), code, _ptr(ws), ws.numel(),
+                                        _stream(E.device, stream)))
+        return Kv, Vv
+    st = _epilogue_struct(epilogue, L, B, Nv, Hkv, hd, E.dtype)
     if ws is None:
-        ws = torch.empty(project_visual_kv_workspace(T, d, nl, E.dtype), dtype=torch.uint8,
+        ws = torch.empty(project_visual_kv_ex_workspace(T, d, nl, hd, E.dtype), dtype=torch.uint8,
                          device=E.device)
-    _check(load().dv_project_visual_kv(_ptr(E), _ptr(Z), _ptr(Uw), _ptr(gamma), _ptr(Wk), _ptr(Wv),
+    _check(lib.dv_project_visual_kv_ex(_ptr(E), _ptr(Z), _ptr(Uw), _ptr(gamma), _ptr(Wk), _ptr(Wv),
                                        _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, l0, nl,
-                                       float(eps), code, _ptr(ws), ws.numel(),
+                                       float(eps), ctypes.byref(st), code, _ptr(ws), ws.numel(),
                                        _stream(E.device, stream)))
     return Kv, Vv
 

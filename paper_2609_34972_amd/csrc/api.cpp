@@ -134,11 +134,39 @@ size_t dv_project_visual_kv_workspace(int64_t T, int32_t d, int32_t nl, int32_t 
   return (size_t)nl * kv_ws_layer_bytes(T, d, dtype);
 }
 
-dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
-                               const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
-                               int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
-                               int32_t hd, int32_t l0, int32_t nl, float eps, int32_t dtype,
-                               void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+size_t rope_table_bytes(int64_t T, int32_t hd) { return ((size_t)T * (size_t)hd * 4 + 255) / 256 * 256; }
+
+dv_status check_epilogue(const dv_kv_epilogue* epi, int32_t hd) {
+  if (!epi) return DV_OK;
+  if (epi->k_bias && !aligned16(epi->k_bias)) return fail(DV_ERR_ALIGN, "k_bias is not 16-byte aligned");
+  if (epi->v_bias && !aligned16(epi->v_bias)) return fail(DV_ERR_ALIGN, "v_bias is not 16-byte aligned");
+  if (epi->k_norm) {
+    if (!aligned16(epi->k_norm)) return fail(DV_ERR_ALIGN, "k_norm is not 16-byte aligned");
+    if (!(epi->k_norm_eps >= 0.f) || !std::isfinite(epi->k_norm_eps))
+      return fail(DV_ERR_SHAPE, "k_norm_eps must be finite and >= 0");
+  }
+  if (epi->positions) {
+    if ((reinterpret_cast<uintptr_t>(epi->positions) & 3u) != 0)
+      return fail(DV_ERR_ALIGN, "positions is not 4-byte aligned");
+    const int32_t* sc = epi->rope_sections;
+    if (sc[0] < 0 || sc[1] < 0 || sc[2] < 0 || (int64_t)sc[0] + sc[1] + sc[2] != hd / 2)
+      return fail(DV_ERR_SHAPE, "rope_sections {%d, %d, %d} must be >= 0 and add up to hd/2 = %d",
+                  sc[0], sc[1], sc[2], hd / 2);
+    if (!std::isfinite(epi->rope_theta) || !(epi->rope_theta > 0.f))
+      return fail(DV_ERR_SHAPE, "rope_theta must be finite and > 0");
+  }
+  return DV_OK;
+}
+
+dv_status project_impl(const void* E, const void* Z, const void* Uw, const void* gamma,
+                       const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B, int32_t Nv,
+                       int32_t d, int32_t L, int32_t r, int32_t Hkv, int32_t hd, int32_t l0,
+                       int32_t nl, float eps, const dv_kv_epilogue* epi, int32_t dtype, void* ws,
+                       size_t ws_bytes, hipStream_t stream, const char* name) {
   DV_CHECK(check_dtype(dtype));
   if (B <= 0 || Nv <= 0 || d <= 0 || L <= 0 || r <= 0 || Hkv <= 0 || hd <= 0)
     return fail(DV_ERR_SHAPE, "sizes must be positive (B=%d Nv=%d d=%d L=%d r=%d Hkv=%d hd=%d)", B,
@@ -153,6 +181,7 @@ dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, con
   if (r % 16 != 0) return fail(DV_ERR_UNSUPPORTED, "r=%d must be a multiple of 16", r);
   if (hd != 64 && hd != 128) return fail(DV_ERR_UNSUPPORTED, "hd=%d must be 64 or 128", hd);
   if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(DV_ERR_SHAPE, "eps must be finite and >= 0");
+  DV_CHECK(check_epilogue(epi, hd));
   DV_CHECK(need_ptr(E, "E"));
   DV_CHECK(need_ptr(Z, "Z"));
   DV_CHECK(need_ptr(Uw, "Uw"));
@@ -161,24 +190,72 @@ dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, con
   DV_CHECK(need_ptr(Wv, "Wv"));
   DV_CHECK(need_ptr(Kv, "Kv"));
   DV_CHECK(need_ptr(Vv, "Vv"));
+  const bool rope = epi && epi->positions;
+  const size_t table = rope ? rope_table_bytes(T, hd) : 0;
   const size_t per_layer = kv_ws_layer_bytes(T, d, dtype);
-  if (!ws || ws_bytes < per_layer)
+  if (!ws || ws_bytes < table + per_layer)
     return fail(DV_ERR_WORKSPACE, "workspace of %zu bytes is below the one-layer minimum %zu",
-                ws ? ws_bytes : (size_t)0, per_layer);
+                ws ? ws_bytes : (size_t)0, table + per_layer);
   if (!aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
-  const int group = (int)std::min<size_t>((size_t)nl, ws_bytes / per_layer);
+  dv::KvEpiArgs ea;
+  if (epi) {
+    ea.k_bias = epi->k_bias;
+    ea.v_bias = epi->v_bias;
+    ea.k_norm = epi->k_norm;
+    ea.k_norm_eps = epi->k_norm_eps;
+  }
+  if (rope) {
+    ea.rope = (const float*)ws;
+    hipError_t e = dv::launch_rope_table(epi->positions, B, Nv, hd, epi->rope_sections[0],
+                                         epi->rope_sections[1], epi->rope_theta, (float*)ws, stream);
+    if (e != hipSuccess) return hip_status(e, name);
+  }
+  char* slots = (char*)ws + table;
+  const int group = (int)std::min<size_t>((size_t)nl, (ws_bytes - table) / per_layer);
   const size_t mem_al = ((size_t)T * d * elem_size(dtype) + 255) / 256 * 256;
   for (int g0 = 0; g0 < nl; g0 += group) {
     const int gl = std::min(group, nl - g0);
-    char* base = (char*)ws;
-    void* Mg = base;
-    float* ssq = (float*)(base + (size_t)gl * mem_al);
+    void* Mg = slots;
+    float* ssq = (float*)(slots + (size_t)gl * mem_al);
     hipError_t e = dv::launch_project_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B, Nv, d, r, Hkv, hd,
                                          l0 + g0, gl, eps, dtype == DV_BF16 ? 1 : 0, Mg, ssq,
-                                         (hipStream_t)stream, g_ev, g0 == 0, g0 + gl >= nl);
-    if (e != hipSuccess) return hip_status(e, "dv_project_visual_kv launch");
+                                         stream, g_ev, g0 == 0, g0 + gl >= nl,
+                                         ea.any() ? &ea : nullptr);
+    if (e != hipSuccess) return hip_status(e, name);
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
+                               const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
+                               int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
+                               int32_t hd, int32_t l0, int32_t nl, float eps, int32_t dtype,
+                               void* ws, size_t ws_bytes, void* stream) {
+  return project_impl(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B, Nv, d, L, r, Hkv, hd, l0, nl, eps,
+                      nullptr, dtype, ws, ws_bytes, (hipStream_t)stream,
+                      "dv_project_visual_kv launch");
+}
+
+size_t dv_project_visual_kv_ex_workspace(int64_t T, int32_t d, int32_t nl, int32_t hd,
+                                         int32_t dtype) {
+  if (T <= 0 || d <= 0 || nl <= 0 || (hd != 64 && hd != 128) ||
+      (dtype != DV_F32 && dtype != DV_BF16))
+    return 0;
+  return rope_table_bytes(T, hd) + (size_t)nl * kv_ws_layer_bytes(T, d, dtype);
+}
+
+dv_status dv_project_visual_kv_ex(const void* E, const void* Z, const void* Uw, const void* gamma,
+                                  const void* Wk, const void* Wv, void* Kv, void* Vv, int32_t B,
+                                  int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
+                                  int32_t hd, int32_t l0, int32_t nl, float eps,
+                                  const dv_kv_epilogue* epi, int32_t dtype, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  return project_impl(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B, Nv, d, L, r, Hkv, hd, l0, nl, eps, epi,
+                      dtype, ws, ws_bytes, (hipStream_t)stream, "dv_project_visual_kv_ex launch");
 }
 
 size_t dv_recurrent_visual_kv_workspace(int64_t T, int32_t d, int32_t L, int32_t r,

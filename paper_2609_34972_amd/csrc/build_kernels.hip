@@ -367,13 +367,48 @@ __global__ __launch_bounds__(UpP::NT) void k_up_norm_p(const bf16* __restrict__ 
   }
 }
 
+// Backbone epilogue arguments as the kernels see them (see KvEpiArgs).
+template <typename T>
+struct KvEpi {
+  const T* kb;
+  const T* vb;
+  const T* kn;
+  float kn_eps;
+  const float* rope;
+};
+
+template <typename T>
+static KvEpi<T> epi_dev(const KvEpiArgs* a) {
+  if (!a) return KvEpi<T>{nullptr, nullptr, nullptr, 0.f, nullptr};
+  return KvEpi<T>{(const T*)a->k_bias, (const T*)a->v_bias, (const T*)a->k_norm, a->k_norm_eps,
+                  a->rope};
+}
+
+__device__ __forceinline__ void unpack8(const u32x4 v, float (&x)[8]) {
+  const bf16x8 b = __builtin_bit_cast(bf16x8, v);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = (float)b[e];
+}
+
+__device__ __forceinline__ u32x4 pack8(const float (&x)[8]) {
+  bf16x8 b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) b[e] = (bf16)x[e];
+  return __builtin_bit_cast(u32x4, b);
+}
+
+// EPI adds the backbone epilogue: the bias joins the scaled product before it is rounded to
+// the call dtype (as the backbone's projection would), then the staged head rows of K get the
+// per-head RMSNorm and the rotary embedding (the partner half of a head is read from the
+// staging buffer) before their single final rounding.
+template <bool EPI>
 __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ Mg,
                                                        const float* __restrict__ ssq,
                                                        const bf16* __restrict__ Wk,
                                                        const bf16* __restrict__ Wv,
                                                        bf16* __restrict__ Kv, bf16* __restrict__ Vv,
                                                        int B_, int Nv, int d, int Hkv, int hd,
-                                                       int l0, int np, float eps) {
+                                                       int l0, int np, float eps, KvEpi<bf16> epi) {
   typedef KvP C;
   extern __shared__ __align__(16) unsigned char smem[];
   const int T = B_ * Nv, kv = Hkv * hd, N = 2 * kv;
@@ -425,8 +460,18 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const f32x16& v = acc[a][b];
-        bf16x4 o = {(bf16)(v[4 * q] * rs), (bf16)(v[4 * q + 1] * rs), (bf16)(v[4 * q + 2] * rs),
-                    (bf16)(v[4 * q + 3] * rs)};
+        float y[4] = {v[4 * q] * rs, v[4 * q + 1] * rs, v[4 * q + 2] * rs, v[4 * q + 3] * rs};
+        if constexpr (EPI) {
+          const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
+          const bf16* bias = n < kv ? epi.kb : epi.vb;
+          if (bias && n < N) {
+            float bb[4];
+            load4_bf16(bias + (int64_t)l * kv + (n < kv ? n : n - kv), bb);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) y[u] += bb[u];
+          }
+        }
+        bf16x4 o = {(bf16)y[0], (bf16)y[1], (bf16)y[2], (bf16)y[3]};
         *(u32x2*)(ep + rw * EP + (b * 32 + pipe_col(lane, q)) * 2) = __builtin_bit_cast(u32x2, o);
       }
   }
@@ -440,8 +485,64 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
     const int rw = r0 + lane / LPR;
     const int row = m0 + wm * C::WM + rw;
     const int n = n0 + wn * C::WN + cpiece;
-    if (row >= T || n >= N) continue;
-    const u32x4 v = *(const u32x4*)(ep + rw * EP + cpiece * 2);
+    const bool valid = row < T && n < N;
+    u32x4 v = *(const u32x4*)(ep + rw * EP + cpiece * 2);
+    if constexpr (EPI) {
+      if (epi.kn || epi.rope) {  // uniform: every lane takes the same branch
+        const bool is_k = n < kv;
+        const int ch = (is_k ? n : n - kv) % hd;  // channel of this lane's first column in its head
+        const int half = hd >> 1;
+        float x[8];
+        unpack8(v, x);
+        float sc = 1.f;
+        if (epi.kn) {
+          // Sum of squares over the head: hd/8 lanes hold one head row (16 for hd 128, 8 for 64).
+          float ss = 0.f;
+          if (is_k && valid)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ss += x[e] * x[e];
+          ss += shfl_xor(ss, 1);
+          ss += shfl_xor(ss, 2);
+          ss += shfl_xor(ss, 4);
+          if (hd == 128) ss += shfl_xor(ss, 8);
+          sc = rsqrtf(ss / (float)hd + epi.kn_eps);
+        }
+        if (is_k && valid) {
+          if (epi.kn) {
+            float w[8];
+            unpack8(*(const u32x4*)(epi.kn + (int64_t)l * hd + ch), w);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] *= sc * w[e];
+          }
+          if (epi.rope) {
+            const bool first = ch < half;
+            const int pc = first ? ch + half : ch - half;  // partner channels of this piece
+            float xp[8];
+            unpack8(*(const u32x4*)(ep + rw * EP + (cpiece + pc - ch) * 2), xp);
+            if (epi.kn) {
+              float w[8];
+              unpack8(*(const u32x4*)(epi.kn + (int64_t)l * hd + pc), w);
+#pragma unroll
+              for (int e = 0; e < 8; ++e) xp[e] *= sc * w[e];
+            }
+            const int j0 = first ? ch : pc;
+            const f32x4* cs = (const f32x4*)(epi.rope + ((int64_t)row * half + j0) * 2);
+#pragma unroll
+            for (int e2 = 0; e2 < 4; ++e2) {
+              const f32x4 t = cs[e2];  // (cos, sin) of frequencies j0 + 2 e2 and j0 + 2 e2 + 1
+#pragma unroll
+              for (int u = 0; u < 2; ++u) {
+                const int e = 2 * e2 + u;
+                const float c = t[2 * u], sn = t[2 * u + 1];
+                x[e] = first ? x[e] * c - xp[e] * sn : x[e] * c + xp[e] * sn;
+              }
+            }
+          }
+          v = pack8(x);
+        }
+      }
+    }
+    if (!valid) continue;
     const int bb = row / Nv, ii = row - bb * Nv;
     bf16* out = n < kv ? Kv : Vv;
     const int o = n < kv ? n : n - kv;
@@ -449,6 +550,105 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
     *(u32x4*)(out + ((int64_t)l * B_ + bb) * Hkv * head_stride + (int64_t)h * head_stride +
               (int64_t)ii * hd + c) = v;
   }
+}
+
+// Backbone epilogue as a pass over stored K/V rows, for the paths whose projection kernel does
+// not fuse it (fp32, and bf16 with r not a multiple of 64). One row of hd channels per hd/2
+// lanes: lane j holds the rotary pair (j, j + hd/2) of K (and of V for the bias). The row is
+// read from the call dtype and rounded once at the end.
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void k_kv_epi_post(T* __restrict__ Kv, T* __restrict__ Vv,
+                                                     int B_, int Nv, int Hkv, int l0, int nl,
+                                                     KvEpi<T> epi) {
+  constexpr int HALF = HD / 2, RPW = WAVE / HALF;  // rows per wave
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t rows = (int64_t)nl * B_ * Hkv * Nv;
+  const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * RPW + lane / HALF;
+  const int j = lane % HALF;
+  const bool valid = row < rows;
+  const int64_t rr = valid ? row : 0;
+  const int i = (int)(rr % Nv);
+  const int h = (int)((rr / Nv) % Hkv);
+  const int b = (int)((rr / ((int64_t)Nv * Hkv)) % B_);
+  const int l = l0 + (int)(rr / ((int64_t)Nv * Hkv * B_));
+  const int kv = Hkv * HD;
+  const int64_t at = ((((int64_t)l * B_ + b) * Hkv + h) * Nv + i) * HD;
+  float k1 = 0.f, k2 = 0.f;
+  if (valid) {
+    k1 = to_f32(Kv[at + j]);
+    k2 = to_f32(Kv[at + j + HALF]);
+    if (epi.kb) {
+      k1 += to_f32(epi.kb[(int64_t)l * kv + h * HD + j]);
+      k2 += to_f32(epi.kb[(int64_t)l * kv + h * HD + j + HALF]);
+    }
+    if (epi.vb) {
+      const float v1 = to_f32(Vv[at + j]) + to_f32(epi.vb[(int64_t)l * kv + h * HD + j]);
+      const float v2 = to_f32(Vv[at + j + HALF]) + to_f32(epi.vb[(int64_t)l * kv + h * HD + j + HALF]);
+      Vv[at + j] = from_f32<T>(v1);
+      Vv[at + j + HALF] = from_f32<T>(v2);
+    }
+  }
+  if (epi.kn) {  // uniform
+    float ss = k1 * k1 + k2 * k2;
+#pragma unroll
+    for (int m = 1; m < HALF; m <<= 1) ss += shfl_xor(ss, m);
+    const float sc = rsqrtf(ss / (float)HD + epi.kn_eps);
+    if (valid) {
+      k1 *= sc * to_f32(epi.kn[(int64_t)l * HD + j]);
+      k2 *= sc * to_f32(epi.kn[(int64_t)l * HD + j + HALF]);
+    }
+  }
+  if (!valid) return;
+  if (epi.rope) {
+    const f32x2 cs = *(const f32x2*)(epi.rope + (((int64_t)b * Nv + i) * HALF + j) * 2);
+    const float a = k1 * cs[0] - k2 * cs[1];
+    k2 = k2 * cs[0] + k1 * cs[1];
+    k1 = a;
+  }
+  if (epi.kb || epi.kn || epi.rope) {
+    Kv[at + j] = from_f32<T>(k1);
+    Kv[at + j + HALF] = from_f32<T>(k2);
+  }
+}
+
+// (cos, sin) of the rotary angle for every (token, frequency); fp64 angle and functions.
+__global__ __launch_bounds__(256) void k_rope_table(const int32_t* __restrict__ pos, int B_, int Nv,
+                                                    int half, int s0, int s1, double log_theta,
+                                                    float* __restrict__ table) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t n = (int64_t)B_ * Nv * half;
+  if (idx >= n) return;
+  const int j = (int)(idx % half);
+  const int64_t t = idx / half;
+  const int b = (int)(t / Nv), i = (int)(t - (int64_t)b * Nv);
+  const int a = j < s0 ? 0 : (j < s0 + s1 ? 1 : 2);
+  const double p = (double)pos[((int64_t)b * 3 + a) * Nv + i];
+  const double ang = p * exp(-(double)j / (double)half * log_theta);
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  *(f32x2*)(table + idx * 2) = f32x2{(float)cs, (float)sn};
+}
+
+hipError_t launch_rope_table(const int32_t* pos, int B_, int Nv, int hd, int s0, int s1,
+                             float theta, float* table, hipStream_t s) {
+  const int half = hd / 2;
+  const int64_t n = (int64_t)B_ * Nv * half;
+  k_rope_table<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(pos, B_, Nv, half, s0, s1,
+                                                          log((double)theta), table);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t epi_post_launch(void* Kv, void* Vv, int B_, int Nv, int Hkv, int hd, int l0,
+                                  int nl, const KvEpiArgs* a, hipStream_t s) {
+  const int64_t rows = (int64_t)nl * B_ * Hkv * Nv;
+  const int rows_per_block = 4 * (WAVE / (hd / 2));
+  const unsigned grid = (unsigned)((rows + rows_per_block - 1) / rows_per_block);
+  if (hd == 128)
+    k_kv_epi_post<T, 128><<<grid, 256, 0, s>>>((T*)Kv, (T*)Vv, B_, Nv, Hkv, l0, nl, epi_dev<T>(a));
+  else
+    k_kv_epi_post<T, 64><<<grid, 256, 0, s>>>((T*)Kv, (T*)Vv, B_, Nv, Hkv, l0, nl, epi_dev<T>(a));
+  return hipGetLastError();
 }
 
 template <typename K>
@@ -505,15 +705,15 @@ hipError_t launch_kv_only(const void* Mg, const float* ssq, const void* Wk, cons
   const int T_ = B_ * Nv;
   if (dtype == 1) {
     static bool once = [] {
-      allow_lds(k_kv_proj_p, kKvLdsBytes);
+      allow_lds(k_kv_proj_p<false>, kKvLdsBytes);
       return true;
     }();
     (void)once;
     dim3 gk(cdiv(2 * Hkv * hd, KvP::BN), cdiv(T_, KvP::BM), nl);
     record(ev.kv[0], s);
-    k_kv_proj_p<<<gk, dim3(KvP::NT), kKvLdsBytes, s>>>((const bf16*)Mg, ssq, (const bf16*)Wk,
-                                                        (const bf16*)Wv, (bf16*)Kv, (bf16*)Vv, B_,
-                                                        Nv, d, Hkv, hd, l0, np, eps);
+    k_kv_proj_p<false><<<gk, dim3(KvP::NT), kKvLdsBytes, s>>>(
+        (const bf16*)Mg, ssq, (const bf16*)Wk, (const bf16*)Wv, (bf16*)Kv, (bf16*)Vv, B_, Nv, d,
+        Hkv, hd, l0, np, eps, epi_dev<bf16>(nullptr));
     record(ev.kv[1], s);
     return hipGetLastError();
   }
@@ -531,11 +731,12 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
                                  const void* Wk, const void* Wv, void* Kv, void* Vv, int B_,
                                  int Nv, int d, int r, int Hkv, int hd, int l0, int nl, float eps,
                                  void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
-                                 bool first, bool last) {
+                                 bool first, bool last, const KvEpiArgs* epi) {
   constexpr int kv_lds = kKvLdsBytes;  // stages (or epilogue staging) + row scales
   static_assert(KvP::NT == 2 * KvP::BM, "two threads per row finish the row scales");
   static bool once = [] {
-    allow_lds(k_kv_proj_p, kv_lds);
+    allow_lds(k_kv_proj_p<false>, kv_lds);
+    allow_lds(k_kv_proj_p<true>, kv_lds);
     allow_lds(k_up_norm_p, kUpLdsBytes);
     return true;
   }();
@@ -552,9 +753,14 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
   if (e != hipSuccess) return e;
   dim3 gk(cdiv(2 * Hkv * hd, KvP::BN), cdiv(T_, KvP::BM), nl);
   if (first) record(ev.kv[0], s);
-  k_kv_proj_p<<<gk, dim3(KvP::NT), kv_lds, s>>>((const bf16*)Mg, ssq, (const bf16*)Wk,
-                                                         (const bf16*)Wv, (bf16*)Kv, (bf16*)Vv, B_,
-                                                         Nv, d, Hkv, hd, l0, np, eps);
+  if (epi && epi->any())
+    k_kv_proj_p<true><<<gk, dim3(KvP::NT), kv_lds, s>>>(
+        (const bf16*)Mg, ssq, (const bf16*)Wk, (const bf16*)Wv, (bf16*)Kv, (bf16*)Vv, B_, Nv, d,
+        Hkv, hd, l0, np, eps, epi_dev<bf16>(epi));
+  else
+    k_kv_proj_p<false><<<gk, dim3(KvP::NT), kv_lds, s>>>(
+        (const bf16*)Mg, ssq, (const bf16*)Wk, (const bf16*)Wv, (bf16*)Kv, (bf16*)Vv, B_, Nv, d,
+        Hkv, hd, l0, np, eps, epi_dev<bf16>(nullptr));
   if (last) record(ev.kv[1], s);
   return hipGetLastError();
 }
@@ -564,7 +770,7 @@ static hipError_t kv_launch(const void* E, const void* Z, const void* Uw, const 
                             const void* Wk, const void* Wv, void* Kv, void* Vv, int B_, int Nv,
                             int d, int r, int Hkv, int hd, int l0, int nl, float eps, void* Mg,
                             float* ssq, hipStream_t s, const LaunchEvents& ev, bool first,
-                            bool last) {
+                            bool last, const KvEpiArgs* epi) {
   typedef typename BuildTiles<T>::Up CU;
   typedef typename BuildTiles<T>::KV CK;
   const int T_ = B_ * Nv;
@@ -579,22 +785,24 @@ static hipError_t kv_launch(const void* E, const void* Z, const void* Uw, const 
   if (first) record(ev.kv[0], s);
   k_kv_proj<CK><<<gk, dim3(CK::NT), CK::LDS_BYTES, s>>>((const T*)Mg, ssq, (const T*)Wk, (const T*)Wv, (T*)Kv, (T*)Vv, B_, Nv, d, Hkv, hd, l0, np, eps);
   if (last) record(ev.kv[1], s);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess || !epi || !epi->any()) return e;
+  return epi_post_launch<T>(Kv, Vv, B_, Nv, Hkv, hd, l0, nl, epi, s);
 }
 
 hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
                              const void* Wk, const void* Wv, void* Kv, void* Vv, int B_, int Nv,
                              int d, int r, int Hkv, int hd, int l0, int nl, float eps, int dtype,
                              void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
-                             bool first, bool last) {
+                             bool first, bool last, const KvEpiArgs* epi) {
   if (dtype == 1 && r % 64 == 0)
     return kv_launch_bf16(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv, hd, l0, nl, eps, Mg,
-                          ssq, s, ev, first, last);
+                          ssq, s, ev, first, last, epi);
   if (dtype == 1)
     return kv_launch<bf16>(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv, hd, l0, nl, eps,
-                           Mg, ssq, s, ev, first, last);
+                           Mg, ssq, s, ev, first, last, epi);
   return kv_launch<float>(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv, hd, l0, nl, eps,
-                          Mg, ssq, s, ev, first, last);
+                          Mg, ssq, s, ev, first, last, epi);
 }
 
 }  // namespace dv

@@ -31,13 +31,31 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T, in
 int kv_partials(int d, int r, int dtype);
 int kv_partials_max(int d);
 
+// Backbone epilogue of the visual K/V: projection bias, per-head key RMSNorm and rotary
+// embedding from a prepared table. A null member skips its step.
+struct KvEpiArgs {
+  const void* k_bias = nullptr;  // [L, Hkv*hd], call dtype
+  const void* v_bias = nullptr;  // [L, Hkv*hd], call dtype
+  const void* k_norm = nullptr;  // [L, hd], call dtype
+  float k_norm_eps = 0.f;
+  const float* rope = nullptr;   // [T][hd/2] (cos, sin) pairs from launch_rope_table
+  bool any() const { return k_bias || v_bias || k_norm || rope; }
+};
+
+// cos/sin table of the rotary embedding for every visual token: entry (t, j) for token
+// t = b*Nv + i turns by pos[b][a][i] * theta^(-2j/hd), a = position axis of frequency j
+// (sections s0, s1, s2 of hd/2 frequencies). table holds T*hd/2 (cos, sin) float pairs.
+hipError_t launch_rope_table(const int32_t* pos, int B, int Nv, int hd, int s0, int s1,
+                             float theta, float* table, hipStream_t s);
+
 // Layers l0..l0+nl-1: memory, RMSNorm and K/V projection. Mg holds nl*T*d
-// elements of the call dtype and ssq nl*kv_partials(d)*T floats.
+// elements of the call dtype and ssq nl*kv_partials(d)*T floats. With epi, the backbone
+// epilogue is applied to the projected K/V (fused into the bf16 pipelined kernel).
 hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
                              const void* Wk, const void* Wv, void* Kv, void* Vv, int B, int Nv,
                              int d, int r, int Hkv, int hd, int l0, int nl, float eps, int dtype,
                              void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
-                             bool first_group, bool last_group);
+                             bool first_group, bool last_group, const KvEpiArgs* epi = nullptr);
 
 // K/V projection alone (Eq. 7) for layers l0..l0+nl-1 from a prepared workspace: Mg holds
 // M_l * gamma_l for each layer of the range (call dtype) and ssq np partial sums of M_l^2 per row.

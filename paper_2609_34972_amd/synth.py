@@ -16,6 +16,11 @@ Distributions (weights N(0, 1/fan_in), activations N(0, 1)):
   Q      [L, B, Nq, Hq, hd]    N(0,1)  text queries of each layer
   Kt, Vt [L, B, Hkv, Nkt, hd]  N(0,1)  text key / value cache of each layer
   Kv, Vv [L, B, Hkv, Nv, hd]   N(0,1)  cached visual K/V (decode workload only)
+  k_bias, v_bias [L, Hkv*hd]   0.05 N(0,1)      backbone projection biases
+  k_norm [L, hd]               1 + 0.1 N(0,1)   backbone per-head key norm weight
+  positions [B, 3, Nv] int32   position ids of the visual tokens: p0 + i on every axis for a
+                               single image, or (p0 + frame, p0 + row, p0 + column) for a video
+                               grid (a multimodal rotary embedding's three axes)
 """
 from __future__ import annotations
 
@@ -29,7 +34,7 @@ import torch
 from .configs import Workload
 
 TENSOR_IDS = {"E": 1, "Dw": 2, "Uw": 3, "gamma": 4, "Wk": 5, "Wv": 6, "Q": 7, "Kt": 8,
-              "Vt": 9, "Kv": 10, "Vv": 11}
+              "Vt": 9, "Kv": 10, "Vv": 11, "k_bias": 12, "v_bias": 13, "k_norm": 14}
 
 _THREADS = max(1, min(16, os.cpu_count() or 1))
 
@@ -107,6 +112,32 @@ def make_visual_cache(w: Workload, seed: int = 0,
         "Kv": _per_layer(seed, "Kv", ls, (w.B, w.Hkv, w.Nv, w.hd), 1.0, 0.0, dt),
         "Vv": _per_layer(seed, "Vv", ls, (w.B, w.Hkv, w.Nv, w.hd), 1.0, 0.0, dt),
     }
+
+
+def make_epilogue_weights(w: Workload, seed: int = 0,
+                          layers: Optional[Iterable[int]] = None) -> Dict[str, torch.Tensor]:
+    """Backbone K/V projection biases and per-head key norm weights."""
+    ls = list(range(w.L)) if layers is None else list(layers)
+    dt = torch_dtype(w)
+    return {
+        "k_bias": _per_layer(seed, "k_bias", ls, (w.kv,), 0.05, 0.0, dt),
+        "v_bias": _per_layer(seed, "v_bias", ls, (w.kv,), 0.05, 0.0, dt),
+        "k_norm": _per_layer(seed, "k_norm", ls, (w.hd,), 0.1, 1.0, dt),
+    }
+
+
+def image_positions(B: int, Nv: int, p0: int = 0) -> torch.Tensor:
+    """Positions p0 + i of Nv consecutive visual tokens, repeated on the three axes."""
+    p = torch.arange(Nv, dtype=torch.int32) + p0
+    return p.view(1, 1, Nv).expand(B, 3, Nv).contiguous()
+
+
+def video_positions(B: int, frames: int, rows: int, cols: int, p0: int = 0) -> torch.Tensor:
+    """(p0 + frame, p0 + row, p0 + column) of a frames x rows x cols token grid (row-major)."""
+    f, r, c = torch.meshgrid(torch.arange(frames), torch.arange(rows), torch.arange(cols),
+                             indexing="ij")
+    p = torch.stack([f.reshape(-1), r.reshape(-1), c.reshape(-1)], 0).to(torch.int32) + p0
+    return p.unsqueeze(0).expand(B, 3, frames * rows * cols).contiguous()
 
 
 def as_f64(t: torch.Tensor) -> np.ndarray:

@@ -199,3 +199,58 @@ def test_kept_workspace_rules(lib):
     proj = lib.dv_project_visual_kv_workspace(2304, 4096, 1, BF16)
     assert one == proj + 2304 * 256 * 2 and many == 17 * one
     assert lib.dv_kept_visual_kv_workspace(2304, 4096, 256, 0, BF16) == 0
+
+
+def ex_call(lib, epi=None, ws=FAKE, ws_bytes=None, **over):
+    a = dict(E=FAKE, Z=FAKE, Uw=FAKE, g=FAKE, Wk=FAKE, Wv=FAKE, Kv=FAKE, Vv=FAKE, B=1, Nv=64, d=256,
+             L=4, r=16, Hkv=4, hd=64, l0=0, nl=4, eps=1e-5, dt=F32)
+    a.update(over)
+    if ws_bytes is None:
+        ws_bytes = lib.dv_project_visual_kv_ex_workspace(a["B"] * a["Nv"], a["d"], a["nl"], a["hd"],
+                                                         a["dt"])
+    return lib.dv_project_visual_kv_ex(a["E"], a["Z"], a["Uw"], a["g"], a["Wk"], a["Wv"], a["Kv"],
+                                       a["Vv"], a["B"], a["Nv"], a["d"], a["L"], a["r"], a["Hkv"],
+                                       a["hd"], a["l0"], a["nl"], a["eps"],
+                                       ctypes.byref(epi) if epi is not None else None, a["dt"], ws,
+                                       ws_bytes, None)
+
+
+def epi(**kw):
+    e = _lib._KvEpilogue()
+    e.k_norm_eps, e.rope_theta = 1e-6, 10000.0
+    e.rope_sections = (ctypes.c_int32 * 3)(32, 0, 0)
+    for k, v in kw.items():
+        if k == "sections":
+            e.rope_sections = (ctypes.c_int32 * 3)(*v)
+        else:
+            setattr(e, k, v)
+    return e
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(positions=FAKE, sections=(16, 8, 4)), SHAPE),
+    (dict(positions=FAKE, sections=(40, -8, 0)), SHAPE),
+    (dict(positions=FAKE, rope_theta=0.0), SHAPE),
+    (dict(positions=FAKE, rope_theta=float("inf")), SHAPE),
+    (dict(positions=FAKE + 2), ALIGN),
+    (dict(k_norm=FAKE, k_norm_eps=-1.0), SHAPE),
+    (dict(k_norm=FAKE + 4), ALIGN),
+    (dict(k_bias=FAKE + 8), ALIGN),
+    (dict(v_bias=FAKE + 2), ALIGN),
+])
+def test_project_ex_rejects_bad_epilogue(lib, kw, code):
+    assert ex_call(lib, epi(**kw)) == code
+
+
+def test_project_ex_rejects_like_plain(lib):
+    assert ex_call(lib, epi(), hd=96) == UNSUP
+    assert ex_call(lib, epi(), E=None) == NULL
+    assert ex_call(lib, None, nl=5) == SHAPE
+
+
+def test_project_ex_workspace_includes_rope_table(lib):
+    one = lib.dv_project_visual_kv_ex_workspace(64, 256, 1, 64, F32)
+    assert one == lib.dv_project_visual_kv_workspace(64, 256, 1, F32) + 64 * 64 * 4
+    assert lib.dv_project_visual_kv_ex_workspace(64, 256, 1, 96, F32) == 0
+    # with rotation the table must fit next to one layer slot
+    assert ex_call(lib, epi(positions=FAKE), ws_bytes=one - 1, nl=1) == WS
