@@ -376,6 +376,38 @@ def run_variants(args, w, Eg, wg, tg, peak, f_build, ms_full_step):
             "visual_cache_bytes": 2 * Kv.numel() * Kv.element_size(),
             "visual_cache_bytes_all_layers": 2 * w.L * w.T * w.kv * Kv.element_size()}
         del Kv, Vv, ws, O, wsa
+    # backbone epilogue of the visual K/V: the rotary embedding of the visual keys at their
+    # positions (a multimodal 16/24/24 rotation over a 16 x 32 x 32 video grid plus the K/V
+    # bias for the video workload, 1-D rotation after a 35-token prompt otherwise)
+    from paper_2609_34972_amd import synth
+    video = w.name == "qwen25vl_video"
+    log("[bench] variant: backbone epilogue")
+    Z = torch.empty(w.L, w.T, w.r, dtype=dt, device=dev)
+    Kv = torch.empty(w.L, w.B, w.Hkv, w.Nv, w.hd, dtype=dt, device=dev)
+    Vv = torch.empty_like(Kv)
+    if video:
+        ew = {k: v.to(dev) for k, v in synth.make_epilogue_weights(w).items()}
+        epi = dvl.KVEpilogue(k_bias=ew["k_bias"], v_bias=ew["v_bias"],
+                             positions=synth.video_positions(w.B, 16, 32, 32, 15).to(dev),
+                             rope_sections=(16, 24, 24), rope_theta=1e6)
+        feats = "k/v bias + multimodal rotary embedding (16/24/24, theta 1e6)"
+    else:
+        epi = dvl.KVEpilogue(positions=synth.image_positions(w.B, w.Nv, 35).to(dev))
+        feats = "rotary embedding (theta 1e4) at positions 35..35+Nv-1"
+    ws = torch.empty(dvl.project_visual_kv_ex_workspace(w.T, w.d, w.L, w.hd, dt),
+                     dtype=torch.uint8, device=dev)
+
+    def build(e):
+        dvl.build_visual_memory(Eg, wg["Dw"], Z, act=w.act)
+        dvl.project_visual_kv(Eg, Z, wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv, Vv, eps=w.eps,
+                              ws=ws, epilogue=e)
+
+    t_plain = percentiles(time_calls(lambda: build(None), steps, warm))
+    t_epi = percentiles(time_calls(lambda: build(epi), steps, warm))
+    res["backbone_epilogue"] = {
+        "features": feats, "build_kv_ms": t_epi, "build_kv_ms_plain": t_plain,
+        "overhead_frac": t_epi["median"] / t_plain["median"] - 1.0}
+    del Z, Kv, Vv, ws, epi
     torch.cuda.empty_cache()
     return res
 
