@@ -58,6 +58,8 @@ def _load():
         lib.dvref_text_visual_attention.restype = i32
         lib.dvref_kv_epilogue.argtypes = [P, P] + [i32] * 5 + [P, P, P, f64, ctypes.c_void_p] + [i32] * 3 + [f64]
         lib.dvref_kv_epilogue.restype = i32
+        lib.dvref_delta_rule.argtypes = [P, P, P, P, P] + [i32] * 6
+        lib.dvref_delta_rule.restype = i32
         lib.dvref_attention_weights.argtypes = [P, P, P, P] + [i32] * 8 + [f64, i32, i32, i32]
         lib.dvref_attention_weights.restype = i32
         _lib = lib
@@ -192,6 +194,22 @@ def kv_epilogue(Kv, Vv, k_bias=None, v_bias=None, k_norm=None, kn_eps: float = 1
     if rc != 0:
         raise ValueError("rotary sections must add up to hd/2")
     return Kv, Vv
+
+
+def delta_rule(k, v, alpha, beta, S):
+    """Gated delta-rule write (appendix on linear attention, Eq. 15-16), token by token:
+    S <- alpha_t S, then S <- S + beta_t k_t (v_t - S^T k_t)^T. k [B,Hk,N,dk], v [B,Hv,N,dv],
+    alpha, beta [B,Hv,N], S [B,Hv,dk,dv]; value head h reads key head h // (Hv/Hk).
+    Returns the final state (a new array)."""
+    k, v, alpha, beta = _c(k), _c(v), _c(alpha), _c(beta)
+    S = _c(S).copy()
+    B, Hk, N, dk = k.shape
+    Hv, dv = v.shape[1], v.shape[3]
+    assert v.shape == (B, Hv, N, dv) and alpha.shape == (B, Hv, N) and beta.shape == alpha.shape
+    assert S.shape == (B, Hv, dk, dv)
+    if _load().dvref_delta_rule(_p(k), _p(v), _p(alpha), _p(beta), _p(S), B, Hk, Hv, N, dk, dv) != 0:
+        raise ValueError("Hv must be a multiple of Hk")
+    return S
 
 
 def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, B: int, Nv: int, Hkv: int, hd: int, eps: float):

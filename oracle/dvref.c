@@ -13,6 +13,8 @@
  *   Section 3.2, Eq. 7   visual K/V = W_{K,l} LN_l(M_l), W_{V,l} LN_l(M_l)
  *   Section 3.2, Eq. 9   text queries attend to [K^v; K^t], [V^v; V^t] with the
  *                        causal structure kept for the text part
+ *   Appendix on linear attention, Eq. 15-16: gated delta-rule write of the visual
+ *                        tokens into a Gated DeltaNet recurrent state
  *
  * Readings where the paper is silent (each is listed with its reason in the
  * design notes of the repository):
@@ -199,6 +201,42 @@ int dvref_kv_epilogue(double* Kv, double* Vv, int L, int B, int Hkv, int Nv, int
         k[j] = x1 * cs - x2 * sn;
         k[j + half] = x2 * cs + x1 * sn;
       }
+    }
+  }
+  return 0;
+}
+
+/* Visual write into a linear-attention (Gated DeltaNet) state (appendix on linear attention,
+ * Eq. 15-16), token by token in order, for every sequence b and value head h (key head
+ * h / (Hv/Hk)):
+ *     S <- alpha_t * S                                   (gated decay, Eq. 15)
+ *     S <- S + beta_t * k_t (v_t - S^T k_t)^T            (delta-rule correction, Eq. 16)
+ * k [B,Hk,N,dk], v [B,Hv,N,dv], alpha, beta [B,Hv,N], S [B,Hv,dk,dv] (in/out).
+ * Returns -1 if Hv is not a multiple of Hk, else 0. */
+int dvref_delta_rule(const double* k, const double* v, const double* alpha, const double* beta,
+                     double* S, int B, int Hk, int Hv, int N, int dk, int dv) {
+  if (Hk <= 0 || Hv % Hk != 0) return -1;
+  const int G = Hv / Hk;
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int b = 0; b < B; ++b) {
+    for (int h = 0; h < Hv; ++h) {
+      double* s = S + ((int64_t)b * Hv + h) * dk * dv;
+      double* sk = (double*)malloc(sizeof(double) * (size_t)dv);
+      for (int t = 0; t < N; ++t) {
+        const double* kt = k + (((int64_t)b * Hk + h / G) * N + t) * dk;
+        const double* vt = v + (((int64_t)b * Hv + h) * N + t) * dv;
+        const double a = alpha[((int64_t)b * Hv + h) * N + t];
+        const double be = beta[((int64_t)b * Hv + h) * N + t];
+        for (int64_t e = 0; e < (int64_t)dk * dv; ++e) s[e] *= a;
+        for (int j = 0; j < dv; ++j) {
+          double acc = 0.0;
+          for (int i = 0; i < dk; ++i) acc += s[(int64_t)i * dv + j] * kt[i];
+          sk[j] = acc;
+        }
+        for (int i = 0; i < dk; ++i)
+          for (int j = 0; j < dv; ++j) s[(int64_t)i * dv + j] += be * kt[i] * (vt[j] - sk[j]);
+      }
+      free(sk);
     }
   }
   return 0;

@@ -440,3 +440,90 @@ def test_rotated_visual_keys_shift_invariant_attention():
         qr = qr[0].transpose(0, 2, 1, 3)
         return oracle.text_visual_attention(qr, kv[0], Vv[0], kt[0], Vt[0], 0)
     np.testing.assert_allclose(run(0), run(777), rtol=1e-11, atol=1e-12)
+
+
+# ---- gated delta-rule visual write (appendix on linear attention, Eq. 15-16) ----
+
+def _unit(a):
+    return a / np.linalg.norm(a, axis=-1, keepdims=True)
+
+
+def test_delta_rule_identity_and_pure_decay():
+    B, Hk, Hv, N, dk, dv = 1, 2, 4, 5, 8, 6
+    k, v = _unit(rnd(90, B, Hk, N, dk)), rnd(91, B, Hv, N, dv)
+    S0 = rnd(92, B, Hv, dk, dv)
+    one, zero = np.ones((B, Hv, N)), np.zeros((B, Hv, N))
+    assert np.array_equal(oracle.delta_rule(k, v, one, zero, S0), S0)
+    a = np.random.default_rng(93).uniform(0.5, 1.0, (B, Hv, N))
+    np.testing.assert_allclose(oracle.delta_rule(k, v, a, zero, S0),
+                               S0 * a.prod(-1)[..., None, None], rtol=1e-13)
+
+
+def test_delta_rule_single_write_from_zero_is_rank_one():
+    B, H, dk, dv = 2, 3, 8, 5
+    k, v = rnd(94, B, H, 1, dk), rnd(95, B, H, 1, dv)
+    beta = np.random.default_rng(96).uniform(0, 1, (B, H, 1))
+    S = oracle.delta_rule(k, v, np.full((B, H, 1), 0.7), beta, np.zeros((B, H, dk, dv)))
+    ref = beta[..., None] * np.einsum("bhi,bhj->bhij", k[:, :, 0], v[:, :, 0])
+    np.testing.assert_allclose(S, ref, rtol=1e-13, atol=1e-15)
+
+
+def test_delta_rule_retrieves_the_last_written_value():
+    # With beta = 1 and a unit key, the state maps the key written last to its value exactly
+    # (the delta rule replaces the old association), whatever was stored before.
+    B, H, N, dk, dv = 1, 2, 6, 16, 8
+    k, v = _unit(rnd(97, B, H, N, dk)), rnd(98, B, H, N, dv)
+    a = np.random.default_rng(99).uniform(0.8, 1.0, (B, H, N))
+    S = rnd(100, B, H, dk, dv)
+    for t in range(N):
+        sl = slice(t, t + 1)
+        S = oracle.delta_rule(k[:, :, sl], v[:, :, sl], a[:, :, sl], np.ones((B, H, 1)), S)
+        np.testing.assert_allclose(np.einsum("bhij,bhi->bhj", S, k[:, :, t]), v[:, :, t],
+                                   rtol=1e-12, atol=1e-12)
+
+
+def test_delta_rule_orthonormal_keys_store_scaled_values():
+    # Distinct basis-vector keys never interfere: row i of S holds beta_t v_t for the token
+    # whose key is e_i (alpha = 1, S_0 = 0).
+    B, H, N, dk, dv = 1, 1, 5, 8, 3
+    k = np.zeros((B, H, N, dk))
+    for t in range(N):
+        k[0, 0, t, (3 * t) % dk] = 1.0
+    v = rnd(101, B, H, N, dv)
+    beta = np.random.default_rng(102).uniform(0, 1, (B, H, N))
+    S = oracle.delta_rule(k, v, np.ones((B, H, N)), beta, np.zeros((B, H, dk, dv)))
+    ref = np.zeros((dk, dv))
+    for t in range(N):
+        ref[(3 * t) % dk] = beta[0, 0, t] * v[0, 0, t]
+    np.testing.assert_allclose(S[0, 0], ref, rtol=1e-14, atol=1e-15)
+
+
+def test_delta_rule_is_affine_in_the_initial_state_and_groups_heads():
+    B, Hk, Hv, N, dk, dv = 1, 2, 4, 7, 8, 4
+    k, v = _unit(rnd(103, B, Hk, N, dk)), rnd(104, B, Hv, N, dv)
+    rng = np.random.default_rng(105)
+    a, beta = rng.uniform(0.6, 1, (B, Hv, N)), rng.uniform(0, 1, (B, Hv, N))
+    S0 = rnd(106, B, Hv, dk, dv)
+    f = lambda S: oracle.delta_rule(k, v, a, beta, S)
+    z = f(np.zeros_like(S0))
+    np.testing.assert_allclose(f(2 * S0) - z, 2 * (f(S0) - z), rtol=1e-11, atol=1e-12)
+    # value head h reads key head h // 2: same as repeating the key heads
+    krep = np.repeat(k, Hv // Hk, axis=1)
+    np.testing.assert_allclose(oracle.delta_rule(krep, v, a, beta, S0), f(S0), rtol=1e-14)
+
+
+def test_delta_rule_orthonormal_keys_decay_after_their_write():
+    # With distinct basis-vector keys, the row of token t's key holds beta_t v_t decayed by the
+    # gates of the later tokens only: prod_{s > t} alpha_s (Eq. 15 applies before each write).
+    B, H, N, dk, dv = 1, 1, 6, 8, 3
+    k = np.zeros((B, H, N, dk))
+    for t in range(N):
+        k[0, 0, t, (5 * t + 1) % dk] = 1.0
+    v = rnd(107, B, H, N, dv)
+    rng = np.random.default_rng(108)
+    alpha, beta = rng.uniform(0.3, 1, (B, H, N)), rng.uniform(0, 1, (B, H, N))
+    S = oracle.delta_rule(k, v, alpha, beta, np.zeros((B, H, dk, dv)))
+    ref = np.zeros((dk, dv))
+    for t in range(N):
+        ref[(5 * t + 1) % dk] = beta[0, 0, t] * v[0, 0, t] * np.prod(alpha[0, 0, t + 1:])
+    np.testing.assert_allclose(S[0, 0], ref, rtol=1e-13, atol=1e-15)
