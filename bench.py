@@ -73,12 +73,15 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="llava7b",
-                   choices=["llava7b", "llava_next", "qwen25vl_video", "decode", "tiny"])
+                   choices=["llava7b", "llava_next", "qwen25vl_video", "decode", "tiny",
+                            "gdn_video", "gdn_image"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the decode-shape measurement appended to prefill workloads")
     p.add_argument("--no-cold", action="store_true",
                    help="skip the cold-cache steps (512 MiB rewritten before each)")
+    p.add_argument("--no-delta", action="store_true",
+                   help="skip the linear-attention visual write appended to prefill workloads")
     p.add_argument("--no-variants", action="store_true",
                    help="skip the recurrent-adapter and layer-skipping measurements")
     p.add_argument("--calibrate-copy", action="store_true",
@@ -412,6 +415,75 @@ def run_variants(args, w, Eg, wg, tg, peak, f_build, ms_full_step):
     return res
 
 
+def run_delta(args, w, steps=None, warmup=None):
+    """Visual write into the linear-attention states of a hybrid Gated DeltaNet backbone
+    (appendix on linear attention): dv_delta_rule_write for every linear-attention layer."""
+    import torch
+
+    import paper_2609_34972_amd as dvl
+    from paper_2609_34972_amd import configs
+
+    steps = steps if steps is not None else args.steps
+    warmup = warmup if warmup is not None else args.warmup
+    dev = torch.device("cuda:0")
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    log(f"[bench] generating {w.name} inputs for {w.layers} layers on the GPU")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    rn = lambda *s: torch.randn(*s, generator=gen, device=dev, dtype=torch.float32)
+    layers = []
+    for _ in range(w.layers):
+        k = rn(w.B, w.Hk, w.N, w.dk)
+        k = (k / k.norm(dim=-1, keepdim=True)).to(dt)
+        layers.append({"k": k, "v": rn(w.B, w.Hv, w.N, w.dv).to(dt),
+                       "alpha": torch.exp(-0.1 * torch.nn.functional.softplus(rn(w.B, w.Hv, w.N))),
+                       "beta": torch.sigmoid(rn(w.B, w.Hv, w.N)),
+                       "S": 0.1 * rn(w.B, w.Hv, w.dk, w.dv)})
+    ws = torch.empty(dvl.delta_rule_workspace(w.B, w.Hv, w.N, w.dk, w.dv, dt), dtype=torch.uint8,
+                     device=dev)
+
+    def step(ev=None):
+        for l, x in enumerate(layers):
+            if ev is not None:
+                dvl.time_kernel(dvl.KERNEL_DELTA_PREP, *ev[l][0])
+                dvl.time_kernel(dvl.KERNEL_DELTA_SCAN, *ev[l][1])
+            dvl.delta_rule_write(x["k"], x["v"], x["alpha"], x["beta"], x["S"], ws=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    hev = HipEvents()
+    evs = [[(hev.pair(), hev.pair()) for _ in range(w.layers)] for _ in range(steps)]
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    marks = [mk() for _ in range(steps + 1)]
+    for s_ in range(steps):
+        marks[s_].record()
+        step(evs[s_])
+    marks[-1].record()
+    torch.cuda.synchronize()
+    dvl.time_kernel(dvl.KERNEL_DELTA_PREP)
+    dvl.time_kernel(dvl.KERNEL_DELTA_SCAN)
+    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(steps)]
+    prep = sum(hev.ms(e[0]) for st in evs for e in st) / (steps * w.layers)
+    scan = sum(hev.ms(e[1]) for st in evs for e in st) / (steps * w.layers)
+    hev.close()
+    ms = percentiles(step_ms)
+    per_layer = ms["median"] / w.layers
+    nbytes = configs.bytes_delta_write(w)
+    res = {"workload": w.name, "layers": w.layers, "batch": w.B, "tokens": w.N,
+           "key_heads": w.Hk, "value_heads": w.Hv, "dk": w.dk, "dv": w.dv,
+           "ms_per_step": ms, "ms_per_layer": per_layer, "prep_kernel_ms": prep,
+           "scan_kernel_ms": scan,
+           "visual_tokens_per_s": w.B * w.N / (ms["median"] * 1e-3),
+           "algorithmic_bytes_per_layer": nbytes,
+           "gbs": nbytes / (per_layer * 1e-3) / 1e9,
+           "hbm_frac": nbytes / (per_layer * 1e-3) / 1e9 / PEAK_HBM_GBS,
+           "recurrence_tflops": configs.flops_delta_write(w) / (per_layer * 1e-3) / 1e12}
+    del layers, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def run_decode(args, w, layers_timed=None):
     """Decode: one new text token per sequence reading every layer's cached visual and text K/V."""
     import torch
@@ -484,6 +556,27 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.workload in ("gdn_video", "gdn_image"):
+        w = configs.GDN_VIDEO if args.workload == "gdn_video" else configs.GDN_IMAGE
+        d = run_delta(args, w)
+        out = {
+            "metric": METRIC, "value": d["visual_tokens_per_s"],
+            "unit": f"visual tokens/s written into {w.layers} linear-attention layers",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": d["ms_per_step"]["median"], "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+            "config": {"workload": w.name, "batch": w.B, "visual_tokens": w.N,
+                       "key_heads": w.Hk, "value_heads": w.Hv, "dk": w.dk, "dv": w.dv,
+                       "layers": w.layers},
+            "roofline": {"bound": "hbm", "kernel": "k_gdr_prep + k_gdr_scan",
+                         "achieved": d["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": d["hbm_frac"], "traffic": None,
+                         "algorithmic_bytes_per_launch": d["algorithmic_bytes_per_layer"],
+                         "ms_per_launch": d["ms_per_layer"]},
+            "delta_write": d,
+        }
+        print(json.dumps(out), flush=True)
+        return
     w = configs.get(args.workload)
     if w.decode:
         d = run_decode(args, w)
@@ -506,6 +599,8 @@ def main():
         out = run_prefill(args, w)
         if not args.no_decode:
             out["decode"] = run_decode(args, configs.DECODE)
+        if not args.no_delta:
+            out["delta_write"] = run_delta(args, configs.GDN_VIDEO, steps=5, warmup=1)
     if args.calibrate_copy:
         n = 1 << 30
         src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)

@@ -203,6 +203,31 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
                                    size_t ws_bytes, void* stream);
 
 /*
+ * Visual write into a linear-attention (Gated DeltaNet) recurrent state (appendix on linear
+ * attention, Eq. 15-16): for every sequence b and value head h, the visual tokens t = 0..N-1
+ * are written in order,
+ *     S <- alpha_t S,   then   S <- S + beta_t k_t (v_t - S^T k_t)^T,
+ * where value head h uses key head h / (Hv/Hk). k, v, alpha and beta come from the backbone's
+ * own norm, projections, causal convolution and gates applied to the visual memories; only
+ * the final state is produced (visual positions take the next layer's memory instead of the
+ * layer outputs).
+ *   k      [B, Hk, N, dk]  call dtype
+ *   v      [B, Hv, N, dv]  call dtype
+ *   alpha  [B, Hv, N]      fp32 gates in (0, 1] (values <= 0 act as the smallest positive float)
+ *   beta   [B, Hv, N]      fp32 write strengths
+ *   S      [B, Hv, dk, dv] fp32 state, read and overwritten in place
+ *   dk, dv in {64, 128}; N may be 0 (nothing is launched)
+ *   ws     at least dv_delta_rule_workspace(B, Hv, N, dk, dv, dtype) bytes
+ * Chunks of 64 tokens are prepared in parallel and then applied in order; the products with
+ * the state read it rounded to the call dtype while the state itself stays fp32.
+ */
+size_t dv_delta_rule_workspace(int32_t B, int32_t Hv, int32_t N, int32_t dk, int32_t dv,
+                               int32_t dtype);
+dv_status dv_delta_rule_write(const void* k, const void* v, const float* alpha, const float* beta,
+                              float* S, int32_t B, int32_t Hk, int32_t Hv, int32_t N, int32_t dk,
+                              int32_t dv, int32_t dtype, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Profiling hook. Kernels of the library, as named by dv_kernel:
  *   DV_KERNEL_DOWN       the all-layer down-projection of dv_build_visual_memory, or the
  *                        whole per-layer adapter chain of dv_recurrent_visual_kv
@@ -211,6 +236,8 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
  *                        dv_recurrent_visual_kv
  *   DV_KERNEL_ATTENTION  the main attention kernel of dv_text_visual_attention
  *                        (without the split-merge kernel)
+ *   DV_KERNEL_DELTA_PREP the per-chunk preparation of dv_delta_rule_write
+ *   DV_KERNEL_DELTA_SCAN the in-order chunk scan of dv_delta_rule_write
  * After dv_time_kernel(k, begin, end) with two hipEvent_t handles, every launch
  * of kernel k made by later calls on this thread is bracketed by
  * hipEventRecord(begin) and hipEventRecord(end) on the call's stream; when a
@@ -222,7 +249,9 @@ typedef enum {
   DV_KERNEL_DOWN = 0,
   DV_KERNEL_UP = 1,
   DV_KERNEL_KV = 2,
-  DV_KERNEL_ATTENTION = 3
+  DV_KERNEL_ATTENTION = 3,
+  DV_KERNEL_DELTA_PREP = 4,
+  DV_KERNEL_DELTA_SCAN = 5
 } dv_kernel;
 dv_status dv_time_kernel(int32_t kernel, void* ev_begin, void* ev_end);
 

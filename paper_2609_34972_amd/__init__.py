@@ -7,8 +7,10 @@ queries attend over all visual keys plus their own causal context (Section 3.2,
 Eq. 9). The arithmetic runs in hand-written HIP kernels behind the C ABI of
 ``include/deltavision.h``; this package only marshals tensors into it.
 """
-from ._lib import (ACT_GELU, ACT_SILU, KERNEL_ATTENTION, KERNEL_DOWN, KERNEL_KV, KERNEL_UP,
-                   DeltaVisionError, KVEpilogue, build_visual_memory, kept_visual_kv,
+from ._lib import (ACT_GELU, ACT_SILU, KERNEL_ATTENTION, KERNEL_DELTA_PREP, KERNEL_DELTA_SCAN,
+                   KERNEL_DOWN, KERNEL_KV, KERNEL_UP,
+                   DeltaVisionError, KVEpilogue, build_visual_memory, delta_rule_workspace,
+                   delta_rule_write, kept_visual_kv,
                    kept_visual_kv_workspace, load, project_visual_kv, project_visual_kv_ex_workspace,
                    project_visual_kv_workspace, recurrent_visual_kv,
                    recurrent_visual_kv_workspace, text_visual_attention,
@@ -21,5 +23,6 @@ __all__ = [
     "recurrent_visual_kv_workspace", "kept_visual_kv", "kept_visual_kv_workspace",
     "text_visual_attention",
     "text_visual_attention_workspace", "time_kernel", "KERNEL_DOWN", "KERNEL_UP", "KERNEL_KV",
-    "KERNEL_ATTENTION",
+    "KERNEL_ATTENTION", "KERNEL_DELTA_PREP", "KERNEL_DELTA_SCAN", "delta_rule_write",
+    "delta_rule_workspace",
 ]

@@ -38,6 +38,8 @@ EXPORTS = (
     "dv_kept_visual_kv",
     "dv_project_visual_kv_ex_workspace",
     "dv_project_visual_kv_ex",
+    "dv_delta_rule_workspace",
+    "dv_delta_rule_write",
 )
 
 
@@ -63,6 +65,7 @@ class KVEpilogue:
     rope_theta: float = 10000.0
 
 KERNEL_DOWN, KERNEL_UP, KERNEL_KV, KERNEL_ATTENTION = 0, 1, 2, 3
+KERNEL_DELTA_PREP, KERNEL_DELTA_SCAN = 4, 5
 
 _lock = threading.Lock()
 _lib = None
@@ -97,6 +100,10 @@ def load() -> ctypes.CDLL:
         lib.dv_project_visual_kv_ex_workspace.restype = sz
         lib.dv_project_visual_kv_ex.argtypes = ([vp] * 8 + [i32] * 9 + [f32, ctypes.POINTER(_KvEpilogue), i32, vp, sz, vp])
         lib.dv_project_visual_kv_ex.restype = i32
+        lib.dv_delta_rule_workspace.argtypes = [i32] * 6
+        lib.dv_delta_rule_workspace.restype = sz
+        lib.dv_delta_rule_write.argtypes = [vp] * 5 + [i32] * 7 + [vp, sz, vp]
+        lib.dv_delta_rule_write.restype = i32
         lib.dv_text_visual_attention_workspace.argtypes = [i32] * 7
         lib.dv_text_visual_attention_workspace.restype = sz
         lib.dv_text_visual_attention.argtypes = [vp] * 6 + [i32] * 8 + [f32, i32, vp, sz, vp]
@@ -299,6 +306,34 @@ def kept_visual_kv(E, Dw, Uw, gamma, Wk, Wv, keep, Kv, Vv, eps: float, act: int 
                                     Nv, d, L, r, Hkv, hd, act, float(eps), code, _ptr(ws),
                                     ws.numel(), _stream(E.device, stream)))
     return Kv, Vv
+
+
+def delta_rule_workspace(B: int, Hv: int, N: int, dk: int, dv: int, dtype: torch.dtype) -> int:
+    code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
+    return int(load().dv_delta_rule_workspace(B, Hv, N, dk, dv, code))
+
+
+def delta_rule_write(k, v, alpha, beta, S, ws: Optional[torch.Tensor] = None, stream=None):
+    """Gated delta-rule write of N tokens into the fp32 state S [B,Hv,dk,dv] in place.
+    k [B,Hk,N,dk], v [B,Hv,N,dv] (call dtype); alpha, beta [B,Hv,N] fp32."""
+    B, Hk, N, dk = k.shape
+    Hv, dv = v.shape[1], v.shape[3]
+    if (tuple(v.shape) != (B, Hv, N, dv) or tuple(alpha.shape) != (B, Hv, N)
+            or beta.shape != alpha.shape or tuple(S.shape) != (B, Hv, dk, dv)):
+        raise ValueError("shape mismatch in delta_rule_write")
+    if alpha.dtype != torch.float32 or beta.dtype != torch.float32 or S.dtype != torch.float32:
+        raise ValueError("alpha, beta and S must be float32")
+    for t in (alpha, beta, S):
+        if not t.is_contiguous() or t.device.type != "cuda":
+            raise ValueError("alpha, beta and S must be contiguous device tensors")
+    code = _dtype_code(k, v)
+    if ws is None:
+        n = delta_rule_workspace(B, Hv, N, dk, dv, k.dtype)
+        ws = torch.empty(max(n, 16), dtype=torch.uint8, device=k.device)
+    _check(load().dv_delta_rule_write(_ptr(k), _ptr(v), alpha.data_ptr(), beta.data_ptr(),
+                                      S.data_ptr(), B, Hk, Hv, N, dk, dv, code, _ptr(ws),
+                                      ws.numel(), _stream(k.device, stream)))
+    return S
 
 
 def text_visual_attention_workspace(B: int, Hq: int, Hkv: int, hd: int, Nv: int, Nq: int,

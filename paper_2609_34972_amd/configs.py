@@ -120,3 +120,43 @@ def bytes_attention(w: Workload, layers: Optional[int] = None) -> float:
     q = w.B * w.Nq * w.Hq * w.hd
     kv = 2 * w.B * w.Hkv * (w.Nv + w.Nkt) * w.hd
     return float((2 * q + kv) * e) * L
+
+
+@dataclass(frozen=True)
+class DeltaWorkload:
+    """Visual write into the linear-attention layers of a hybrid Gated DeltaNet backbone
+    (appendix on linear attention): N visual tokens of B sequences written into the state of
+    Hv value heads (key heads Hk) in each of `layers` linear-attention layers."""
+    name: str
+    dtype: str
+    B: int
+    Hk: int
+    Hv: int
+    N: int
+    dk: int
+    dv: int
+    layers: int
+
+    def with_(self, **kw) -> "DeltaWorkload":
+        return replace(self, **kw)
+
+
+# 24 linear-attention layers with 16 key / 32 value heads of 128 channels (a 4B-class hybrid
+# backbone with 8 full-attention layers); a 576-token image batch and a 16384-token video.
+GDN_IMAGE = DeltaWorkload("gdn_image", "bf16", B=4, Hk=16, Hv=32, N=576, dk=128, dv=128, layers=24)
+GDN_VIDEO = DeltaWorkload("gdn_video", "bf16", B=1, Hk=16, Hv=32, N=16384, dk=128, dv=128,
+                          layers=24)
+
+
+def bytes_delta_write(w: DeltaWorkload) -> float:
+    """Bytes read once and written once by the visual write of one layer: k, v, the gates and
+    the fp32 state in and out."""
+    e = 2 if w.dtype == "bf16" else 4
+    return (w.B * w.N * (w.Hk * w.dk + w.Hv * w.dv) * e + 2 * w.B * w.Hv * w.N * 4
+            + 2 * w.B * w.Hv * w.dk * w.dv * 4)
+
+
+def flops_delta_write(w: DeltaWorkload) -> float:
+    """Arithmetic of the token-by-token recurrence for one layer: per token and value head, the
+    decay (dk dv), the read-out S^T k (2 dk dv) and the rank-one update (3 dk dv)."""
+    return 6.0 * w.B * w.Hv * w.N * w.dk * w.dv

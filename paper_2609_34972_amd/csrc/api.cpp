@@ -12,6 +12,7 @@
 
 #include "attention.hpp"
 #include "build_kernels.hpp"
+#include "delta_rule.hpp"
 
 namespace {
 
@@ -102,6 +103,8 @@ dv_status dv_time_kernel(int32_t kernel, void* ev_begin, void* ev_end) {
     case DV_KERNEL_UP: slot = g_ev.up; break;
     case DV_KERNEL_KV: slot = g_ev.kv; break;
     case DV_KERNEL_ATTENTION: slot = g_ev.attn; break;
+    case DV_KERNEL_DELTA_PREP: slot = g_ev.gdr_prep; break;
+    case DV_KERNEL_DELTA_SCAN: slot = g_ev.gdr_scan; break;
     default: return fail(DV_ERR_UNSUPPORTED, "unknown kernel id %d", kernel);
   }
   slot[0] = (hipEvent_t)ev_begin;
@@ -387,6 +390,43 @@ dv_status dv_kept_visual_kv(const void* E, const void* Dw, const void* Uw, const
     a = b;
   }
   return ok();
+}
+
+size_t dv_delta_rule_workspace(int32_t B, int32_t Hv, int32_t N, int32_t dk, int32_t dv,
+                               int32_t dtype) {
+  if (B <= 0 || Hv <= 0 || N <= 0 || (dk != 64 && dk != 128) || (dv != 64 && dv != 128) ||
+      (dtype != DV_F32 && dtype != DV_BF16))
+    return 0;
+  return dv::gdr_layout(nullptr, B, Hv, N, dk, dv, dtype == DV_BF16 ? 1 : 0).bytes;
+}
+
+dv_status dv_delta_rule_write(const void* k, const void* v, const float* alpha, const float* beta,
+                              float* S, int32_t B, int32_t Hk, int32_t Hv, int32_t N, int32_t dk,
+                              int32_t dv, int32_t dtype, void* ws, size_t ws_bytes, void* stream) {
+  DV_CHECK(check_dtype(dtype));
+  if (B <= 0 || Hk <= 0 || Hv <= 0 || N < 0)
+    return fail(DV_ERR_SHAPE, "B=%d Hk=%d Hv=%d must be positive and N=%d >= 0", B, Hk, Hv, N);
+  if (Hv % Hk != 0) return fail(DV_ERR_SHAPE, "Hv=%d is not a multiple of Hk=%d", Hv, Hk);
+  if (B > 65535 || Hv > 65535) return fail(DV_ERR_SHAPE, "B and Hv must be at most 65535");
+  if ((dk != 64 && dk != 128) || (dv != 64 && dv != 128))
+    return fail(DV_ERR_UNSUPPORTED, "dk=%d and dv=%d must be 64 or 128", dk, dv);
+  DV_CHECK(need_ptr(S, "S"));
+  if (N == 0) return ok();
+  DV_CHECK(need_ptr(k, "k"));
+  DV_CHECK(need_ptr(v, "v"));
+  if (!alpha || !beta) return fail(DV_ERR_NULL, "alpha and beta must not be NULL");
+  if ((reinterpret_cast<uintptr_t>(alpha) & 3u) || (reinterpret_cast<uintptr_t>(beta) & 3u))
+    return fail(DV_ERR_ALIGN, "alpha and beta must be 4-byte aligned");
+  const int bf = dtype == DV_BF16 ? 1 : 0;
+  const size_t need = dv::gdr_layout(nullptr, B, Hv, N, dk, dv, bf).bytes;
+  if (!ws || ws_bytes < need)
+    return fail(DV_ERR_WORKSPACE, "workspace of %zu bytes is below the required %zu",
+                ws ? ws_bytes : (size_t)0, need);
+  if (!aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
+  const dv::GdrWs w = dv::gdr_layout(ws, B, Hv, N, dk, dv, bf);
+  return hip_status(dv::launch_delta_rule(k, v, alpha, beta, S, B, Hk, Hv, N, dk, dv, bf, w,
+                                          (hipStream_t)stream, g_ev),
+                    "dv_delta_rule_write launch");
 }
 
 size_t dv_text_visual_attention_workspace(int32_t B, int32_t Hq, int32_t Hkv, int32_t hd,

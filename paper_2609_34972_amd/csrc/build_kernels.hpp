@@ -16,6 +16,8 @@ struct LaunchEvents {
   hipEvent_t up[2] = {nullptr, nullptr};
   hipEvent_t kv[2] = {nullptr, nullptr};
   hipEvent_t attn[2] = {nullptr, nullptr};
+  hipEvent_t gdr_prep[2] = {nullptr, nullptr};
+  hipEvent_t gdr_scan[2] = {nullptr, nullptr};
 };
 
 inline void record(hipEvent_t e, hipStream_t s) {

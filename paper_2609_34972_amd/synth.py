@@ -18,6 +18,9 @@ Distributions (weights N(0, 1/fan_in), activations N(0, 1)):
   Kv, Vv [L, B, Hkv, Nv, hd]   N(0,1)  cached visual K/V (decode workload only)
   k_bias, v_bias [L, Hkv*hd]   0.05 N(0,1)      backbone projection biases
   k_norm [L, hd]               1 + 0.1 N(0,1)   backbone per-head key norm weight
+  delta-rule inputs            k [B,Hk,N,dk] unit rows (as the backbone normalises its keys),
+                               v [B,Hv,N,dv] N(0,1), alpha = exp(-0.1 softplus(N(0,1))),
+                               beta = sigmoid(N(0,1)), initial state S [B,Hv,dk,dv] 0.1 N(0,1)
   positions [B, 3, Nv] int32   position ids of the visual tokens: p0 + i on every axis for a
                                single image, or (p0 + frame, p0 + row, p0 + column) for a video
                                grid (a multimodal rotary embedding's three axes)
@@ -34,7 +37,8 @@ import torch
 from .configs import Workload
 
 TENSOR_IDS = {"E": 1, "Dw": 2, "Uw": 3, "gamma": 4, "Wk": 5, "Wv": 6, "Q": 7, "Kt": 8,
-              "Vt": 9, "Kv": 10, "Vv": 11, "k_bias": 12, "v_bias": 13, "k_norm": 14}
+              "Vt": 9, "Kv": 10, "Vv": 11, "k_bias": 12, "v_bias": 13, "k_norm": 14,
+              "dr_k": 15, "dr_v": 16, "dr_alpha": 17, "dr_beta": 18, "dr_S": 19}
 
 _THREADS = max(1, min(16, os.cpu_count() or 1))
 
@@ -138,6 +142,23 @@ def video_positions(B: int, frames: int, rows: int, cols: int, p0: int = 0) -> t
                              indexing="ij")
     p = torch.stack([f.reshape(-1), r.reshape(-1), c.reshape(-1)], 0).to(torch.int32) + p0
     return p.unsqueeze(0).expand(B, 3, frames * rows * cols).contiguous()
+
+
+def make_delta_inputs(w, seed: int = 0) -> Dict[str, torch.Tensor]:
+    """Inputs of the gated delta-rule write of a DeltaWorkload (see the module docstring)."""
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    k = normal(seed, "dr_k", 0, (w.B, w.Hk, w.N, w.dk))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    z = normal(seed, "dr_alpha", 0, (w.B, w.Hv, w.N)).astype(np.float64)
+    alpha = np.exp(-0.1 * np.logaddexp(0.0, z)).astype(np.float32)
+    beta = (1.0 / (1.0 + np.exp(-normal(seed, "dr_beta", 0, (w.B, w.Hv, w.N))))).astype(np.float32)
+    return {
+        "k": _to_dtype(k, dt),
+        "v": _to_dtype(normal(seed, "dr_v", 0, (w.B, w.Hv, w.N, w.dv)), dt),
+        "alpha": torch.from_numpy(alpha),
+        "beta": torch.from_numpy(beta),
+        "S": torch.from_numpy(0.1 * normal(seed, "dr_S", 0, (w.B, w.Hv, w.dk, w.dv))),
+    }
 
 
 def as_f64(t: torch.Tensor) -> np.ndarray:

@@ -254,3 +254,36 @@ def test_project_ex_workspace_includes_rope_table(lib):
     assert lib.dv_project_visual_kv_ex_workspace(64, 256, 1, 96, F32) == 0
     # with rotation the table must fit next to one layer slot
     assert ex_call(lib, epi(positions=FAKE), ws_bytes=one - 1, nl=1) == WS
+
+
+def dr_call(lib, ws=FAKE, ws_bytes=None, **over):
+    a = dict(k=FAKE, v=FAKE, alpha=FAKE, beta=FAKE, S=FAKE, B=1, Hk=2, Hv=4, N=100, dk=64, dv=64,
+             dt=F32)
+    a.update(over)
+    if ws_bytes is None:
+        ws_bytes = lib.dv_delta_rule_workspace(a["B"], a["Hv"], max(a["N"], 1), a["dk"], a["dv"],
+                                               a["dt"])
+    return lib.dv_delta_rule_write(a["k"], a["v"], a["alpha"], a["beta"], a["S"], a["B"], a["Hk"],
+                                   a["Hv"], a["N"], a["dk"], a["dv"], a["dt"], ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), NULL), (dict(v=None), NULL), (dict(alpha=None), NULL), (dict(S=None), NULL),
+    (dict(S=FAKE + 4), ALIGN), (dict(beta=FAKE + 2), ALIGN), (dict(k=FAKE + 8), ALIGN),
+    (dict(B=0), SHAPE), (dict(Hk=0), SHAPE), (dict(N=-1), SHAPE), (dict(Hk=3), SHAPE),
+    (dict(dk=96), UNSUP), (dict(dv=32), UNSUP), (dict(dt=2), UNSUP),
+    (dict(ws=None), WS), (dict(ws_bytes=256), WS), (dict(ws=FAKE + 8), ALIGN),
+])
+def test_delta_rule_rejects(lib, kw, code):
+    assert dr_call(lib, **kw) == code
+
+
+def test_delta_rule_without_tokens_is_a_no_op(lib):
+    assert dr_call(lib, N=0, k=None, v=None, alpha=None, beta=None, ws=None, ws_bytes=0) == OK
+
+
+def test_delta_rule_workspace_scales_with_chunks(lib):
+    one = lib.dv_delta_rule_workspace(1, 32, 64, 128, 128, BF16)
+    assert one >= 32 * (64 * 128 * 3 * 2 + 4)
+    assert lib.dv_delta_rule_workspace(1, 32, 65, 128, 128, BF16) > one  # a second chunk
+    assert lib.dv_delta_rule_workspace(1, 32, 64, 96, 128, BF16) == 0
