@@ -281,8 +281,12 @@ constexpr int ROWB = HD * 2;              // bytes per K/V row
 constexpr int TILE_BYTES = KT * ROWB;     // one tensor's tile: 16 KiB
 constexpr int STAGE_BYTES = 2 * TILE_BYTES;
 // Stages: up to two tiles keep loading while one is computed. A wave counts at most 63
-// outstanding loads (6-bit vmcnt), i.e. two tiles of a single-wave block.
-template <int NW> constexpr int stages() { return 3; }
+// outstanding loads (6-bit vmcnt), i.e. two tiles of a single-wave block. Four-wave blocks
+// keep two stages (64 KiB of LDS) so that two blocks share a CU: one block's softmax (VALU)
+// then overlaps the other's MFMA work.
+template <int NW> constexpr int stages() { return NW == 4 ? 2 : 3; }
+// Streaming blocks that fit in one CU's 160 KiB of LDS.
+template <int NW> constexpr int blocks_per_cu() { return (160 * 1024) / (stages<NW>() * 2 * 64 * 256); }
 template <int NW> constexpr int lds_bytes() { return stages<NW>() * STAGE_BYTES; }
 constexpr int BLOCKS_PER_TILE = KT / 4;   // 1 KiB (4-row) load instructions per tensor
 // XOR keys of the 16-byte chunks of a 256-byte LDS row. K rows are read whole-chunk by 16 rows
@@ -343,7 +347,7 @@ __device__ __forceinline__ void stream_sync(int ahead) {
 }
 
 template <int NW>
-__global__ __launch_bounds__(NW * 64) void k_attn_stream(AttnArgs a, int row_blocks) {
+__global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnArgs a, int row_blocks) {
   using namespace stream;
   constexpr int NS = stages<NW>();
   constexpr int INS = 2 * BLOCKS_PER_TILE / NW;  // load instructions per wave per tile
@@ -1003,8 +1007,25 @@ AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt,
   int64_t want = units >= min_blocks ? 1 : cdiv64(min_blocks, units);
   want = std::min<int64_t>(want, std::max<int64_t>(1, tiles / 2));
   want = std::max<int64_t>(1, std::min<int64_t>(want, 64));
-  if (want > 1 && per_split > 0) {
-    const int64_t fit = (int64_t)(ws_bytes / (size_t)per_split);
+  const int64_t fit = per_split > 0 ? (int64_t)(ws_bytes / (size_t)per_split) : 0;
+  const int64_t slots = 256 * (p.nw == 4 ? stream::blocks_per_cu<4>()
+                                         : (p.nw == 2 ? stream::blocks_per_cu<2>()
+                                                      : stream::blocks_per_cu<1>()));
+  if (p.stream && !p.ksplit && units < slots) {
+    // Streaming blocks are LDS-bound (one or two per CU), so they run in rounds of `slots`:
+    // take the split count with the fewest tile steps over all rounds,
+    // rounds(units * S) * ceil(tiles / S), preferring fewer splits on ties.
+    int64_t best = 1, best_cost = tiles;
+    const int64_t smax = std::min<int64_t>(64, std::max<int64_t>(1, tiles / 2));
+    for (int64_t sp = 2; sp <= smax && sp <= fit; ++sp) {
+      const int64_t cost = cdiv64(units * sp, slots) * cdiv64(tiles, sp);
+      if (cost < best_cost) {
+        best = sp;
+        best_cost = cost;
+      }
+    }
+    want = best;
+  } else if (want > 1 && per_split > 0) {
     want = std::min<int64_t>(want, fit);
     if (want < 2) want = 1;
   }
