@@ -12,7 +12,10 @@
 //                    memory times gamma_l for the K/V projection and the RMSNorm partial sums.
 // The K/V projection of all layers then runs as one launch of the embedding path's kernel.
 // The state stays fp32 for every dtype so rounding does not accumulate over the layers.
+// bf16 runs with r a multiple of 64 use the pipelined direct-to-LDS engine (k_*_p kernels);
+// fp32 runs and other ranks use the register-staged engine.
 #include "build_kernels.hpp"
+#include "gemm_pipe.hpp"
 #include "gemm_tile.hpp"
 
 namespace dv {
@@ -138,6 +141,153 @@ __global__ __launch_bounds__(C::NT) void k_up_rec(const TIn* Min, float* Mst,
   }
 }
 
+// ------------------------------------------------------------------ pipelined bf16 kernels
+
+typedef PipeCfg<128, 128, 2, 2> RecP;
+// Up-projection epilogue staging: the fp32 tile, rows padded by 4 floats.
+constexpr int kRecPitch = RecP::BN + 4;
+constexpr int kRecLds = RecP::BM * kRecPitch * 4 > RecP::LDS_BYTES ? RecP::BM * kRecPitch * 4
+                                                                   : RecP::LDS_BYTES;
+
+// partial[s][t][j] = sum over k in split s of X[t][k] * Dw_l[j][k]  (one 128x128 tile, one split)
+__global__ __launch_bounds__(RecP::NT) void k_down_partial_p(const bf16* __restrict__ X,
+                                                             const bf16* __restrict__ Dl,
+                                                             float* __restrict__ part, int T, int d,
+                                                             int r, int kchunk) {
+  typedef RecP C;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int s = blockIdx.z;
+  const int k0 = s * kchunk, klen = min(kchunk, d - k0);
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const int ldb = d * 2;
+  // Bases at (first row, first column of the split); the byte ranges end with the matrices,
+  // so rows past the end read as zeros.
+  BufOperand A{buffer_rsrc(X + (int64_t)m0 * d + k0, (int64_t)(T - m0) * ldb - (int64_t)k0 * 2),
+               buffer_rsrc(X, 0), 1 << 30, ldb};
+  BufOperand B{buffer_rsrc(Dl + (int64_t)n0 * d + k0, (int64_t)(r - n0) * ldb - (int64_t)k0 * 2),
+               buffer_rsrc(Dl, 0), 1 << 30, ldb};
+  f32x16 acc[C::FM][C::FN];
+  pipe_mainloop<C>(A, B, klen, (bf16*)smem, acc);
+  const int lane = threadIdx.x & 63, wave = wave_index();
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  float* ps = part + (int64_t)s * T * r;
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a) {
+    const int row = m0 + wm * C::WM + a * 32 + (lane & 31);
+    if (row >= T) continue;
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
+        if (col >= r) continue;
+        const f32x16& v = acc[a][b];
+        *(f32x4*)(ps + (int64_t)row * r + col) = f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+      }
+  }
+}
+
+// Eight consecutive values of the previous memory as fp32 (bf16 E or the fp32 state).
+struct Prev8 {
+  f32x4 lo, hi;
+};
+__device__ __forceinline__ Prev8 load_prev8(const bf16* p) {
+  const bf16x8 v = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
+  return Prev8{f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]},
+               f32x4{(float)v[4], (float)v[5], (float)v[6], (float)v[7]}};
+}
+__device__ __forceinline__ Prev8 load_prev8(const float* p) {
+  return Prev8{*(const f32x4*)p, *(const f32x4*)(p + 4)};
+}
+
+// M_l = Min + Z_l U_l for a 128 x 128 tile. Min (E or the fp32 state, which it may alias) is
+// fetched before the main loop; the fp32 product goes through padded LDS so that 16 lanes cover
+// each 128-column row, and every output moves as whole pieces of a row: the fp32 state, its
+// bf16 copy (the next layer's down-projection operand), M * gamma and the row's sum of squares
+// over this column tile.
+template <typename TIn>
+__global__ __launch_bounds__(RecP::NT) void k_up_rec_p(const TIn* Min, float* Mst,
+                                                       bf16* __restrict__ Mop,
+                                                       const bf16* __restrict__ Z,
+                                                       const bf16* __restrict__ Ul,
+                                                       const bf16* __restrict__ gl,
+                                                       bf16* __restrict__ Mg,
+                                                       float* __restrict__ ssq, int T, int d, int r) {
+  typedef RecP C;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  constexpr int kRows = C::BM / (C::NT / 16);
+  const int c8 = (threadIdx.x & 15) * 8;
+  const int r16 = threadIdx.x >> 4;
+  const bool col_ok = n0 + c8 < d;
+  Prev8 prev[kRows];
+#pragma unroll
+  for (int i = 0; i < kRows; ++i) {
+    const int row = m0 + r16 + i * (C::NT / 16);
+    prev[i] = (row < T && col_ok) ? load_prev8(Min + (int64_t)row * d + n0 + c8) : Prev8{};
+  }
+  const int ldb = r * 2;
+  BufOperand A{buffer_rsrc(Z + (int64_t)m0 * r, (int64_t)(T - m0) * ldb), buffer_rsrc(Z, 0),
+               1 << 30, ldb};
+  BufOperand B{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
+               1 << 30, ldb};
+  f32x16 acc[C::FM][C::FN];
+  pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
+
+  const int lane = threadIdx.x & 63, wave = wave_index();
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  float* tile = (float*)smem;  // the main loop's last LDS read precedes its last barrier
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a) {
+    const int rl = wm * C::WM + a * 32 + (lane & 31);
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = wn * C::WN + b * 32 + pipe_col(lane, q);
+        const f32x16& v = acc[a][b];
+        *(f32x4*)(tile + rl * kRecPitch + c) = f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+      }
+  }
+  __syncthreads();
+  bf16x8 g8 = {};
+  if (col_ok) g8 = __builtin_bit_cast(bf16x8, *(const u32x4*)(gl + n0 + c8));
+#pragma unroll
+  for (int i = 0; i < kRows; ++i) {
+    const int rr = r16 + i * (C::NT / 16);
+    const int row = m0 + rr;
+    float ss = 0.f;
+    if (row < T && col_ok) {
+      const int64_t at = (int64_t)row * d + n0 + c8;
+      const f32x4 p0 = *(const f32x4*)(tile + rr * kRecPitch + c8);
+      const f32x4 p1 = *(const f32x4*)(tile + rr * kRecPitch + c8 + 4);
+      f32x4 m0v, m1v;
+      bf16x8 o, mg;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        m0v[u] = p0[u] + prev[i].lo[u];
+        m1v[u] = p1[u] + prev[i].hi[u];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float m = u < 4 ? m0v[u] : m1v[u - 4];
+        ss += m * m;
+        o[u] = (bf16)m;
+        mg[u] = (bf16)(m * (float)g8[u]);
+      }
+      *(f32x4*)(Mst + at) = m0v;
+      *(f32x4*)(Mst + at + 4) = m1v;
+      if (Mop) *(u32x4*)(Mop + at) = __builtin_bit_cast(u32x4, o);
+      *(u32x4*)(Mg + at) = __builtin_bit_cast(u32x4, mg);
+    }
+    ss += shfl_xor(ss, 1);
+    ss += shfl_xor(ss, 2);
+    ss += shfl_xor(ss, 4);
+    ss += shfl_xor(ss, 8);
+    if ((threadIdx.x & 15) == 0 && row < T) ssq[(int64_t)blockIdx.x * T + row] = ss;
+  }
+}
+
 // ------------------------------------------------------------------ host side
 
 static const int kMaxSplits = 16;
@@ -187,6 +337,15 @@ static hipError_t rec_launch(const void* E, const void* Dw, const void* Uw, cons
   T* Z = (T*)(base + w.z);
   float* part = (float*)(base + w.part);
   const int kchunk = w.kchunk;
+  const bool pipelined = std::is_same<T, bf16>::value && r % 64 == 0;
+  static bool once = [] {
+    (void)hipFuncSetAttribute((const void*)k_up_rec_p<bf16>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kRecLds);
+    (void)hipFuncSetAttribute((const void*)k_up_rec_p<float>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kRecLds);
+    return true;
+  }();
+  (void)once;
   const int64_t nz = (int64_t)T_ * r;
   dim3 gd(rcdiv(r, C::BN), rcdiv(T_, C::BM), w.splits);
   dim3 gu(rcdiv(d, C::BN), rcdiv(T_, C::BM));
@@ -195,8 +354,12 @@ static hipError_t rec_launch(const void* E, const void* Dw, const void* Uw, cons
     // Operand of this layer's down projection: E for the first layer, then the previous
     // memory (its rounded copy for bf16 runs, the fp32 state itself for fp32 runs).
     const T* X = l == 0 ? (const T*)E : (op ? (const T*)op : (const T*)state);
-    k_down_partial<C><<<gd, dim3(C::NT), C::LDS_BYTES, s>>>(X, (const T*)Dw + (int64_t)l * r * d,
-                                                            part, T_, d, r, kchunk);
+    if (pipelined)
+      k_down_partial_p<<<gd, dim3(RecP::NT), RecP::LDS_BYTES, s>>>(
+          (const bf16*)X, (const bf16*)Dw + (int64_t)l * r * d, part, T_, d, r, kchunk);
+    else
+      k_down_partial<C><<<gd, dim3(C::NT), C::LDS_BYTES, s>>>(X, (const T*)Dw + (int64_t)l * r * d,
+                                                              part, T_, d, r, kchunk);
     if (act == 0)
       k_reduce_act<T, 0><<<rcdiv(nz, 256), 256, 0, s>>>(part, Z, nz, w.splits);
     else
@@ -205,7 +368,15 @@ static hipError_t rec_launch(const void* E, const void* Dw, const void* Uw, cons
     const T* gl = (const T*)gamma + (int64_t)l * d;
     T* Mgl = Mg + (int64_t)l * T_ * d;
     float* ssql = ssq + (int64_t)l * w.np * T_;
-    if (l == 0)
+    if (pipelined && l == 0)
+      k_up_rec_p<bf16><<<gu, dim3(RecP::NT), kRecLds, s>>>(
+          (const bf16*)E, state, (bf16*)op, (const bf16*)Z, (const bf16*)Ul, (const bf16*)gl,
+          (bf16*)Mgl, ssql, T_, d, r);
+    else if (pipelined)
+      k_up_rec_p<float><<<gu, dim3(RecP::NT), kRecLds, s>>>(
+          state, state, (bf16*)op, (const bf16*)Z, (const bf16*)Ul, (const bf16*)gl, (bf16*)Mgl,
+          ssql, T_, d, r);
+    else if (l == 0)
       k_up_rec<C, T><<<gu, dim3(C::NT), C::LDS_BYTES, s>>>((const T*)E, state, op, Z, Ul, gl, Mgl,
                                                            ssql, T_, d, r);
     else
