@@ -280,18 +280,22 @@ __global__ __launch_bounds__(DownP::NT) void k_down_act_p(const bf16* __restrict
 // Up-projection epilogue staging: the fp32 tile, rows padded by 4 floats so the transposed
 // accumulator writes (32 rows at one column per instruction) hit distinct banks.
 constexpr int kUpPitch = UpP::BN + 4;
-constexpr int kUpLdsBytes = UpP::BM * kUpPitch * 4 > UpP::LDS_BYTES ? UpP::BM * kUpPitch * 4
-                                                                     : UpP::LDS_BYTES;
+template <class C>
+constexpr int up_lds_bytes() {
+  return C::BM * (C::BN + 4) * 4 > C::LDS_BYTES ? C::BM * (C::BN + 4) * 4 : C::LDS_BYTES;
+}
+constexpr int kUpLdsBytes = up_lds_bytes<UpP>();
 
-__global__ __launch_bounds__(UpP::NT) void k_up_norm_p(const bf16* __restrict__ E,
+template <class C>
+__global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        const bf16* __restrict__ Z,
                                                        const bf16* __restrict__ Uw,
                                                        const bf16* __restrict__ gamma,
                                                        bf16* __restrict__ Mg,
                                                        float* __restrict__ ssq, int T, int d,
                                                        int r, int l0) {
-  typedef UpP C;
   extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int kUpPitch = C::BN + 4;
   const int lz = blockIdx.z, l = l0 + lz;
   const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
   const bf16* Zl = Z + (int64_t)l * T * r;
@@ -737,7 +741,7 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
   static bool once = [] {
     allow_lds(k_kv_proj_p<false>, kv_lds);
     allow_lds(k_kv_proj_p<true>, kv_lds);
-    allow_lds(k_up_norm_p, kUpLdsBytes);
+    allow_lds(k_up_norm_p<UpP>, kUpLdsBytes);
     return true;
   }();
   (void)once;
@@ -745,9 +749,9 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
   const int np = cdiv(d, UpP::BN);
   dim3 gu(np, cdiv(T_, UpP::BM), nl);
   if (first) record(ev.up[0], s);
-  k_up_norm_p<<<gu, dim3(UpP::NT), kUpLdsBytes, s>>>((const bf16*)E, (const bf16*)Z,
-                                                         (const bf16*)Uw, (const bf16*)gamma,
-                                                         (bf16*)Mg, ssq, T_, d, r, l0);
+  k_up_norm_p<UpP><<<gu, dim3(UpP::NT), kUpLdsBytes, s>>>(
+      (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_, d, r,
+      l0);
   if (last) record(ev.up[1], s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
