@@ -18,7 +18,9 @@
 // itself stays fp32.
 #include "delta_rule.hpp"
 
+#include <algorithm>
 #include <cfloat>
+#include <cmath>
 
 #include "dv_device.hpp"
 
@@ -276,6 +278,11 @@ struct ScanLds {
   static constexpr size_t bytes = ush + (size_t)32 * (C + P) * sizeof(T);
 };
 
+// The chunk step S <- gamma_C S + Kt (Uv - W S) is affine in S, so a run of chunks maps a
+// start state S to Phi S + Psi. A long sequence is cut into ws.P segments: k_gdr_scan_seg runs
+// every segment at once from the start states I (for Phi, without Uv) and 0 (for Psi), and
+// k_gdr_combine_seg then applies the segments in order, S <- Phi_g S + Psi_g. With one segment
+// k_gdr_scan reads and writes S directly.
 template <typename T, int DK, int DV>
 __global__ __launch_bounds__(gdr::NT) void k_gdr_scan(float* __restrict__ S, int Hv, int N,
                                                       GdrWs ws) {
@@ -372,6 +379,196 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_scan(float* __restrict__ S, int
   }
 }
 
+// Two-level scan kernels for dk = dv = 128: one block owns all 128 columns of its state (the
+// Phi block or the Psi block of a segment, or the state in the combine), so every chunk's W and
+// Kt are read once per block. Wave w keeps state rows [32 w, 32 w + 32) of all four column
+// tiles; the U tiles (2 token tiles x 4 column tiles) are shared out two per wave.
+template <typename T>
+struct FullLds {
+  static constexpr int C = gdr::C, P = gdr::PAD;
+  static constexpr size_t ssh = 0;                                        // T[128][128+P]
+  static constexpr size_t ush = ssh + (size_t)128 * (128 + P) * sizeof(T);  // T[128][C+P]
+  static constexpr size_t bytes = ush + (size_t)128 * (C + P) * sizeof(T);
+};
+
+template <typename T>
+__global__ __launch_bounds__(gdr::NT) void k_gdr_scan_seg(int Hv, int N, GdrWs ws) {
+  using namespace gdr;
+  typedef typename Frag8<T>::type F;
+  typedef FullLds<T> L;
+  constexpr int DK = 128, DV = 128, NCT = 4;  // column tiles of 32
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* Ssh = (T*)(smem + L::ssh);  // [column][dk]
+  T* Ush = (T*)(smem + L::ush);  // [column][token]
+  constexpr int SP = DK + PAD, UP = C + PAD;
+  const int P = ws.P;
+  const bool phi = blockIdx.x == 0;
+  const int hv = blockIdx.y, b = blockIdx.z / P, seg = blockIdx.z - b * P;
+  const int NC = (N + C - 1) / C;
+  const int c_begin = seg * ws.cps, c_end = min(NC, c_begin + ws.cps);
+  const int64_t seq = (int64_t)b * Hv + hv;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 5, rr = lane & 31;
+  const int ut = wave & 1;        // token tile of this wave's U tiles
+  const int uc0 = wave >> 1;      // its U column tiles: uc0 and uc0 + 2
+
+  f32x16 st[NCT];
+#pragma unroll
+  for (int j = 0; j < NCT; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      st[j][i] = (phi && wave * 32 + acc_row(lane, i) == j * 32 + rr) ? 1.f : 0.f;
+
+  F wf[DK / 16], kf[C / 16];
+  T uv[2][16];
+  float gcn = 1.f;
+  auto fetch = [&](int c) {
+    const int64_t cid = seq * NC + c;
+    gcn = ws.gc[cid];
+    const T* W = ws.w<T>(cid, DK) + (int64_t)(ut * 32 + rr) * DK;
+#pragma unroll
+    for (int ks = 0; ks < DK / 16; ++ks) wf[ks] = *(const F*)(W + ks * 16 + h * 8);
+    const T* Kt = ws.kt<T>(cid, DK) + (int64_t)(wave * 32 + rr) * C;
+#pragma unroll
+    for (int ks = 0; ks < C / 16; ++ks) kf[ks] = *(const F*)(Kt + ks * 16 + h * 8);
+    if (!phi) {
+      const T* Uv = ws.uv<T>(cid, DV) + (int64_t)(ut * 32) * DV + uc0 * 32 + rr;
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) uv[q][i] = Uv[(int64_t)acc_row(lane, i) * DV + q * 64];
+    }
+  };
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) uv[q][i] = from_f32<T>(0.f);
+  if (c_begin < c_end) fetch(c_begin);
+  for (int c = c_begin; c < c_end; ++c) {
+    F wnow[DK / 16], know[C / 16];
+    T unow[2][16];
+#pragma unroll
+    for (int q = 0; q < DK / 16; ++q) wnow[q] = wf[q];
+#pragma unroll
+    for (int q = 0; q < C / 16; ++q) know[q] = kf[q];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) unow[q][i] = uv[q][i];
+    const float gc = gcn;
+    if (c + 1 < c_end) fetch(c + 1);
+    // (a) publish the state in the call dtype
+#pragma unroll
+    for (int j = 0; j < NCT; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        Ssh[(j * 32 + rr) * SP + wave * 32 + acc_row(lane, i)] = from_f32<T>(st[j][i]);
+    __syncthreads();
+    // (b) U = Uv - W S: this wave's two tiles (token tile ut, column tiles uc0, uc0 + 2)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int uc = uc0 + 2 * q;
+      f32x16 a0 = {}, a1 = {};
+#pragma unroll
+      for (int ks = 0; ks < DK / 16; ks += 2) {
+        mfma_k16(a0, wnow[ks], *(const F*)(Ssh + (uc * 32 + rr) * SP + ks * 16 + h * 8));
+        mfma_k16(a1, wnow[ks + 1], *(const F*)(Ssh + (uc * 32 + rr) * SP + (ks + 1) * 16 + h * 8));
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        Ush[(uc * 32 + rr) * UP + ut * 32 + acc_row(lane, i)] =
+            from_f32<T>(to_f32(unow[q][i]) - (a0[i] + a1[i]));
+      }
+    }
+    __syncthreads();
+    // (c) S = gamma_C S + Kt U for all four column tiles of this wave's rows
+#pragma unroll
+    for (int j = 0; j < NCT; ++j) {
+      f32x16 p0 = {}, p1 = {};
+#pragma unroll
+      for (int ks = 0; ks < C / 16; ks += 2) {
+        mfma_k16(p0, know[ks], *(const F*)(Ush + (j * 32 + rr) * UP + ks * 16 + h * 8));
+        mfma_k16(p1, know[ks + 1], *(const F*)(Ush + (j * 32 + rr) * UP + (ks + 1) * 16 + h * 8));
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) st[j][i] = st[j][i] * gc + (p0[i] + p1[i]);
+    }
+  }
+  float* out = phi ? ws.phi + (seq * P + seg) * DK * DK : ws.psi + (seq * P + seg) * DK * DV;
+#pragma unroll
+  for (int j = 0; j < NCT; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) out[(int64_t)(wave * 32 + acc_row(lane, i)) * 128 + j * 32 + rr] = st[j][i];
+}
+
+// S <- Phi_g S + Psi_g for g = 0 .. P-1, one block per (sequence, value head), all 128 columns.
+template <typename T>
+__global__ __launch_bounds__(gdr::NT) void k_gdr_combine_seg(float* __restrict__ S, int Hv, GdrWs ws) {
+  using namespace gdr;
+  typedef typename Frag8<T>::type F;
+  typedef FullLds<T> L;
+  constexpr int DK = 128, DV = 128, NCT = 4;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* Ssh = (T*)(smem + L::ssh);
+  constexpr int SP = DK + PAD;
+  const int P = ws.P;
+  const int hv = blockIdx.y, b = blockIdx.z;
+  const int64_t seq = (int64_t)b * Hv + hv;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int h = lane >> 5, rr = lane & 31;
+  float* Sg = S + seq * DK * DV;
+  f32x16 st[NCT];
+#pragma unroll
+  for (int j = 0; j < NCT; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) st[j][i] = Sg[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + j * 32 + rr];
+  F af[DK / 16];
+  auto fetch = [&](int g) {
+    const float* Phi = ws.phi + (seq * P + g) * DK * DK + (int64_t)(wave * 32 + rr) * DK;
+#pragma unroll
+    for (int ks = 0; ks < DK / 16; ++ks) {
+      const f32x4 lo = *(const f32x4*)(Phi + ks * 16 + h * 8);
+      const f32x4 hi = *(const f32x4*)(Phi + ks * 16 + h * 8 + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        af[ks][e] = from_f32<T>(lo[e]);
+        af[ks][e + 4] = from_f32<T>(hi[e]);
+      }
+    }
+  };
+  fetch(0);
+  for (int g = 0; g < P; ++g) {
+    F anow[DK / 16];
+#pragma unroll
+    for (int q = 0; q < DK / 16; ++q) anow[q] = af[q];
+    if (g + 1 < P) fetch(g + 1);
+#pragma unroll
+    for (int j = 0; j < NCT; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        Ssh[(j * 32 + rr) * SP + wave * 32 + acc_row(lane, i)] = from_f32<T>(st[j][i]);
+    __syncthreads();
+    const float* Psi = ws.psi + (seq * P + g) * DK * DV;
+#pragma unroll
+    for (int j = 0; j < NCT; ++j) {
+      f32x16 p0 = {}, p1 = {};
+#pragma unroll
+      for (int ks = 0; ks < DK / 16; ks += 2) {
+        mfma_k16(p0, anow[ks], *(const F*)(Ssh + (j * 32 + rr) * SP + ks * 16 + h * 8));
+        mfma_k16(p1, anow[ks + 1], *(const F*)(Ssh + (j * 32 + rr) * SP + (ks + 1) * 16 + h * 8));
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        st[j][i] = (p0[i] + p1[i]) + Psi[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + j * 32 + rr];
+    }
+    __syncthreads();  // every wave is done reading Ssh before the next step rewrites it
+  }
+#pragma unroll
+  for (int j = 0; j < NCT; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) Sg[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + j * 32 + rr] = st[j][i];
+}
+
 template <typename K>
 static void allow_lds_bytes(K kernel, size_t bytes) {
   (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -387,6 +584,10 @@ static hipError_t gdr_launch(const void* k, const void* v, const float* alpha, c
   static bool once = [] {
     allow_lds_bytes(k_gdr_prep<T, DK, DV>, LP::bytes);
     allow_lds_bytes(k_gdr_scan<T, DK, DV>, LS::bytes);
+    if constexpr (DK == 128 && DV == 128) {
+      allow_lds_bytes(k_gdr_scan_seg<T>, FullLds<T>::bytes);
+      allow_lds_bytes(k_gdr_combine_seg<T>, FullLds<T>::bytes);
+    }
     return true;
   }();
   (void)once;
@@ -398,16 +599,56 @@ static hipError_t gdr_launch(const void* k, const void* v, const float* alpha, c
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   record(ev.gdr_scan[0], s);
-  k_gdr_scan<T, DK, DV><<<dim3(DV / 32, Hv, B), gdr::NT, LS::bytes, s>>>(S, Hv, N, ws);
+  if (ws.P > 1) {
+    if constexpr (DK == 128 && DV == 128) {
+      k_gdr_scan_seg<T><<<dim3(2, Hv, B * ws.P), gdr::NT, FullLds<T>::bytes, s>>>(Hv, N, ws);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      k_gdr_combine_seg<T><<<dim3(1, Hv, B), gdr::NT, FullLds<T>::bytes, s>>>(S, Hv, ws);
+    } else {
+      return hipErrorInvalidValue;  // segments are only planned for dk = dv = 128
+    }
+  } else {
+    k_gdr_scan<T, DK, DV><<<dim3(DV / 32, Hv, B), gdr::NT, LS::bytes, s>>>(S, Hv, N, ws);
+  }
   record(ev.gdr_scan[1], s);
   return hipGetLastError();
 }
 
+// Segments of the two-level scan, from a latency model of the two schedules (times per chunk
+// step measured on MI355X at dk = dv = 128): the plain scan runs every chunk in order at about
+// 1.5 us a step with DV / 32 small blocks per sequence; the segmented scan runs ceil(NC / P)
+// steps at about 3.4 us, in as many rounds as its 2 B Hv P one-per-CU blocks need, and the
+// combine adds P steps of about 3.7 us. P = 1 selects the plain scan. The scan's grid dimension
+// B * P stays within 65535.
+static void gdr_segments(int NC, int B, int Hv, int dk, int dv, int& P, int& cps) {
+  P = 1;
+  cps = NC;
+  if (dk != 128 || dv != 128 || NC < 16) return;
+  const double cus = 256.0;
+  const double plain_rounds = std::ceil(B * (double)Hv * (dv / 32) / (cus * 8));
+  double best = plain_rounds * NC * 1.5;
+  const int pmax = std::min(64, std::min(NC / 2, 65535 / B));
+  for (int p = 2; p <= pmax; ++p) {
+    const int c = (NC + p - 1) / p;
+    const int pp = (NC + c - 1) / c;
+    const double rounds = std::ceil(2.0 * B * Hv * pp / cus);
+    const double t = rounds * c * 3.4 + pp * 3.7 * std::ceil(B * (double)Hv / cus);
+    if (t < best) {
+      best = t;
+      P = pp;
+      cps = c;
+    }
+  }
+}
+
 GdrWs gdr_layout(void* base, int B, int Hv, int N, int dk, int dv, int dtype) {
   const size_t e = dtype == 1 ? 2 : 4;
-  const int64_t chunks = (int64_t)B * Hv * ((N + gdr::C - 1) / gdr::C);
+  const int NC = (N + gdr::C - 1) / gdr::C;
+  const int64_t chunks = (int64_t)B * Hv * NC;
   auto al = [](size_t x) { return (x + 255) / 256 * 256; };
   GdrWs w{};
+  gdr_segments(NC, B, Hv, dk, dv, w.P, w.cps);
   char* p = (char*)base;
   size_t o = 0;
   w.w_ = p ? p + o : nullptr;   o += al((size_t)chunks * gdr::C * dk * e);
@@ -415,6 +656,9 @@ GdrWs gdr_layout(void* base, int B, int Hv, int N, int dk, int dv, int dtype) {
   w.kt_ = p ? p + o : nullptr;  o += al((size_t)chunks * gdr::C * dk * e);
   w.gc = p ? (float*)(p + o) : nullptr;
   o += al((size_t)chunks * 4);
+  const size_t segs = w.P > 1 ? (size_t)B * Hv * w.P : 0;
+  w.phi = p ? (float*)(p + o) : nullptr;  o += al(segs * dk * dk * 4);
+  w.psi = p ? (float*)(p + o) : nullptr;  o += al(segs * dk * dv * 4);
   w.bytes = o;
   return w;
 }

@@ -10,12 +10,17 @@
 namespace dv {
 
 // Workspace of the chunked delta rule: per (sequence, value head, chunk of 64 tokens) the
-// products W [64][dk], Uv [64][dv], Kt [dk][64] in the call dtype and gamma_C (fp32).
+// products W [64][dk], Uv [64][dv], Kt [dk][64] in the call dtype and gamma_C (fp32), and per
+// segment of the two-level scan the affine map (Phi, Psi) in fp32.
 struct GdrWs {
   void* w_;
   void* uv_;
   void* kt_;
   float* gc;
+  float* phi;  // per segment: the linear part Phi [dk][dk] of the segment's affine map
+  float* psi;  // per segment: the state Psi [dk][dv] it reaches from a zero start
+  int P;       // segments of the two-level scan (1: a single in-order scan)
+  int cps;     // chunks per segment
   size_t bytes;
   template <typename T>
   __host__ __device__ T* w(int64_t chunk, int dk) const { return (T*)w_ + chunk * 64 * dk; }

@@ -20,6 +20,10 @@ CASES = [
     configs.GDN_IMAGE.with_(name="dr_bf16_ragged", B=2, Hk=4, Hv=8, N=700),
     configs.GDN_IMAGE.with_(name="dr_bf16_dk64_dv128", B=1, Hk=2, Hv=2, N=333, dk=64, dv=128),
     configs.GDN_IMAGE.with_(name="dr_bf16_image", B=4, Hk=4, Hv=8),
+    # long sequences at dk = dv = 128 take the two-level scan (segments of the affine chunk
+    # map, then the segments in order)
+    SMALL.with_(name="dr_f32_segmented", B=1, Hk=1, Hv=2, N=4000, dk=128, dv=128),
+    configs.GDN_IMAGE.with_(name="dr_bf16_segmented", B=2, Hk=2, Hv=4, N=4096),
 ]
 
 
