@@ -568,7 +568,7 @@ def main():
             "config": {"workload": w.name, "batch": w.B, "visual_tokens": w.N,
                        "key_heads": w.Hk, "value_heads": w.Hv, "dk": w.dk, "dv": w.dv,
                        "layers": w.layers},
-            "roofline": {"bound": "hbm", "kernel": "k_gdr_prep + k_gdr_scan",
+            "roofline": {"bound": "hbm", "kernel": "k_gdr_prep + k_gdr_chain (+ k_gdr_merge)",
                          "achieved": d["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": d["hbm_frac"], "traffic": None,
                          "algorithmic_bytes_per_launch": d["algorithmic_bytes_per_layer"],

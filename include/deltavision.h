@@ -237,7 +237,8 @@ dv_status dv_delta_rule_write(const void* k, const void* v, const float* alpha, 
  *   DV_KERNEL_ATTENTION  the main attention kernel of dv_text_visual_attention
  *                        (without the split-merge kernel)
  *   DV_KERNEL_DELTA_PREP the per-chunk preparation of dv_delta_rule_write
- *   DV_KERNEL_DELTA_SCAN the in-order chunk scan of dv_delta_rule_write
+ *   DV_KERNEL_DELTA_SCAN the in-order chunk chain of dv_delta_rule_write (with the segment merge
+ *                        when the sequence is split into segments)
  * After dv_time_kernel(k, begin, end) with two hipEvent_t handles, every launch
  * of kernel k made by later calls on this thread is bracketed by
  * hipEventRecord(begin) and hipEventRecord(end) on the call's stream; when a

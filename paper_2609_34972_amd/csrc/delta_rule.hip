@@ -11,11 +11,19 @@
 // not depend on the state, and the state after the chunk is
 //     S_C = gamma_C S_0 + Kt U,   Kt = (diag(gamma_C / gamma) K)^T.
 // k_gdr_prep computes Uv, W, Kt and gamma_C for every chunk in parallel (MFMA for K K^T and
-// the two products, fp32 forward substitution for T); k_gdr_scan then runs the chunks in
-// order, U = Uv - W S and S = gamma_C S + Kt U, with the fp32 state in MFMA accumulators. The
-// rule acts on every state column independently, so the scan splits the value columns over
-// workgroups (32 per block). Products read the state rounded to the call dtype; the state
-// itself stays fp32.
+// the two products, fp32 forward substitution for T) and stores them as one record per chunk
+// in fragment order (below). k_gdr_chain then runs the chunks in order, U = Uv - W S and
+// S = gamma_C S + Kt U. The rule acts on every state column independently: each wave keeps 32
+// columns of the fp32 state, all dk rows, in MFMA accumulators, and since those accumulators
+// (and those of U) are already the B operands of the next product in a permuted k order, a
+// wave's chain needs no exchange with other waves; the block only shares the chunk record,
+// copied into LDS one chunk ahead. Products read the state rounded to the call dtype; the
+// state itself stays fp32.
+//
+// Long sequences use a two-level scan. The chunk step is affine in S, so a run of chunks maps
+// a start state S to Phi S + Psi: the segments of ws.cps chunks run at once, from the start
+// state I for Phi (without Uv) and 0 for Psi (segment 0 from S itself), and k_gdr_merge then
+// applies them in order.
 #include "delta_rule.hpp"
 
 #include <algorithm>
@@ -23,6 +31,7 @@
 #include <cmath>
 
 #include "dv_device.hpp"
+#include "gemm_pipe.hpp"
 
 namespace dv {
 
@@ -42,6 +51,67 @@ template <typename T>
 __device__ __forceinline__ typename Frag8<T>::type frag_zero() {
   return typename Frag8<T>::type{};
 }
+
+// Fragment order. One 32x32x16 MFMA step takes from lane half h the 8 values at k = 8 h .. 8 h + 7
+// of its row (A) or column (B); any assignment of the 16 k to (half, slot) pairs works as long as
+// both operands use it. A 32x32 accumulator tile holds in lane half h, items 8 q .. 8 q + 7, the
+// rows 16 q + {4 h .. 4 h + 3, 8 + 4 h .. 8 + 4 h + 3}: so with k assigned the same way, items
+// 8 q .. 8 q + 7 of an accumulator are directly the B fragment of k step q. Matrices meant to
+// meet such accumulators store every row with the index m inside each 16-group moved to
+// position frag_pos(m) (bits 2 and 3 swapped, an involution), so that a lane half's 8 values
+// are contiguous; the 16-byte chunks of a row are XOR-swizzled by the row so that the 16 rows
+// one fragment load touches fall in distinct LDS bank groups.
+__device__ __forceinline__ int frag_pos(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
+
+// Element offset of logical position pos in row `row` of a fragment-order matrix of INNER
+// values per row.
+template <typename T, int INNER>
+__device__ __forceinline__ int frag_off(int row, int pos) {
+  constexpr int EPC = 16 / (int)sizeof(T), CPR = INNER / EPC;
+  static_assert(CPR == 8 || CPR == 16 || CPR == 32, "row of 8, 16 or 32 chunks");
+  const int key = CPR >= 16 ? (row & 15) : ((row >> 1) & 7);
+  return row * INNER + (((pos / EPC) ^ key) * EPC) + pos % EPC;
+}
+
+// The 8 values at logical positions 8 g .. 8 g + 7 of row `row`.
+template <typename T, int INNER>
+__device__ __forceinline__ typename Frag8<T>::type frag_get(const T* m, int row, int g) {
+  typedef typename Frag8<T>::type F;
+  if constexpr (sizeof(T) == 2) {
+    return *(const F*)(m + frag_off<T, INNER>(row, 8 * g));
+  } else {
+    const f32x4 lo = *(const f32x4*)(m + frag_off<T, INNER>(row, 8 * g));
+    const f32x4 hi = *(const f32x4*)(m + frag_off<T, INNER>(row, 8 * g + 4));
+    return F{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  }
+}
+
+template <typename T, int INNER>
+__device__ __forceinline__ void frag_put(T* m, int row, int g, typename Frag8<T>::type x) {
+  typedef typename Frag8<T>::type F;
+  if constexpr (sizeof(T) == 2) {
+    *(F*)(m + frag_off<T, INNER>(row, 8 * g)) = x;
+  } else {
+    *(f32x4*)(m + frag_off<T, INNER>(row, 8 * g)) = f32x4{x[0], x[1], x[2], x[3]};
+    *(f32x4*)(m + frag_off<T, INNER>(row, 8 * g + 4)) = f32x4{x[4], x[5], x[6], x[7]};
+  }
+}
+
+// Items 8 q .. 8 q + 7 of an accumulator tile, rounded to T: a B fragment in fragment order.
+template <typename T>
+__device__ __forceinline__ typename Frag8<T>::type acc_frag(const f32x16& a, int q) {
+  typename Frag8<T>::type x;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = from_f32<T>(a[8 * q + e]);
+  return x;
+}
+
+// Per-chunk record of the workspace: -W [C][DK], Kt [DK][C], Uv^T [DV][C], all in fragment order.
+template <typename T, int DK, int DV>
+struct GdrRec {
+  static constexpr int C = gdr::C;
+  static constexpr int KT = C * DK, UV = 2 * C * DK, ELEMS = C * (2 * DK + DV);
+};
 
 // LDS layout of k_gdr_prep (byte offsets). For bf16, T diag(beta) and T diag(beta gamma)
 // (unpadded rows) reuse the bytes of A, which is dead once A21 T11 is formed; the block then
@@ -204,14 +274,19 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
       if (half == 0) Tf[i * TP + 32 + j] = 0.f;  // upper-right block
     }
   } else {
-    T* Kt = ws.kt<T>(seq * NC + c, DK);
+    // Kt in fragment order: logical positions 8 gq .. 8 gq + 7 of row n hold tokens
+    // frag_pos(8 gq + e), two runs of four.
+    T* Kt = ws.rec<T>(seq * NC + c) + GdrRec<T, DK, DV>::KT;
     for (int idx = tid - 64; idx < DK * (C / 8); idx += NT - 64) {
-      const int n = idx / (C / 8), s0 = (idx % (C / 8)) * 8;
-      const F x = *(const F*)(KT + n * CP + s0);
+      const int n = idx / (C / 8), gq = idx % (C / 8);
+      const int t0 = (gq >> 1) * 16 + (gq & 1) * 4;
       F y;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = from_f32<T>(__expf(gC - g[s0 + e]) * to_f32(x[e]));
-      *(F*)(Kt + n * C + s0) = y;
+      for (int e = 0; e < 8; ++e) {
+        const int t = t0 + (e >> 2) * 8 + (e & 3);
+        y[e] = from_f32<T>(__expf(gC - g[t]) * to_f32(KT[n * CP + t]));
+      }
+      frag_put<T, C>(Kt, n, gq, y);
     }
   }
   __syncthreads();
@@ -243,330 +318,289 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
   }
   __syncthreads();
 
-  // 5. Uv = (T diag(beta)) V and W = (T diag(beta gamma)) K, 32x32 tiles over the waves.
+  // 5. Uv = (T diag(beta)) V and W = (T diag(beta gamma)) K, 32x32 tiles over the waves. Uv
+  //    comes out with a value column per lane and W, computed as K^T (T diag(beta gamma))^T, with
+  //    a token per lane, so both store rows of their fragment-order form (Uv^T and -W): items
+  //    8 q .. 8 q + 7 of a tile are logical positions 16 q + 8 h .. + 7 of the lane's row.
   constexpr int NU = (C / 32) * (DV / 32), NW = (C / 32) * (DK / 32);
-  T* Uv = ws.uv<T>(seq * NC + c, DV);
-  T* W = ws.w<T>(seq * NC + c, DK);
+  T* rec = ws.rec<T>(seq * NC + c);
   for (int q = wave; q < NU + NW; q += NT / 64) {
     const bool isu = q < NU;
     const int qq = isu ? q : q - NU;
     const int nd = isu ? DV / 32 : DK / 32;
     const int ti = qq / nd, ni = qq % nd;
-    const T* As = isu ? Tu : Tw;
-    const T* Bs = isu ? VT : KT;
     f32x16 acc = {};
 #pragma unroll
     for (int ks = 0; ks < C / 16; ++ks) {
       const int ko = ks * 16 + h * 8;
-      mfma_k16(acc, frag_load<T>(As + (ti * 32 + rr) * L::TWP + ko),
-               frag_load<T>(Bs + (ni * 32 + rr) * CP + ko));
+      if (isu)
+        mfma_k16(acc, frag_load<T>(Tu + (ti * 32 + rr) * L::TWP + ko), frag_load<T>(VT + (ni * 32 + rr) * CP + ko));
+      else
+        mfma_k16(acc, frag_load<T>(KT + (ni * 32 + rr) * CP + ko), frag_load<T>(Tw + (ti * 32 + rr) * L::TWP + ko));
     }
-    T* out = isu ? Uv : W;
-    const int ld = isu ? DV : DK;
+    if (isu) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      out[(ti * 32 + acc_row(lane, i)) * ld + ni * 32 + rr] = from_f32<T>(acc[i]);
+      for (int qh = 0; qh < 2; ++qh)
+        frag_put<T, C>(rec + GdrRec<T, DK, DV>::UV, ni * 32 + rr, ti * 4 + 2 * qh + h, acc_frag<T>(acc, qh));
+    } else {
+#pragma unroll
+      for (int qh = 0; qh < 2; ++qh)
+        frag_put<T, DK>(rec, ti * 32 + rr, ni * 4 + 2 * qh + h, acc_frag<T>(-acc, qh));
+    }
   }
   if (tid == 0) ws.gc[seq * NC + c] = __expf(gC);
 }
 
-template <typename T, int DK>
-struct ScanLds {
-  static constexpr int C = gdr::C, P = gdr::PAD;
-  static constexpr size_t ssh = 0;                                       // T[32][DK+P]
-  static constexpr size_t ush = ssh + (size_t)32 * (DK + P) * sizeof(T);  // T[32][C+P]
-  static constexpr size_t bytes = ush + (size_t)32 * (C + P) * sizeof(T);
+// LDS of k_gdr_chain: the chunk records in NS buffers (bf16: three, so that two records are in
+// flight while one is used; fp32: one). Per wave, a record copy is INS_PSI (with Uv) or INS_PHI
+// (without) 1 KiB instructions.
+template <typename T, int DK, int DV>
+struct ChainLds {
+  typedef GdrRec<T, DK, DV> R;
+  static constexpr int NS = sizeof(T) == 2 ? 3 : 1;
+  static constexpr size_t bytes = (size_t)NS * R::ELEMS * sizeof(T);
+  static constexpr int INS_PSI = R::ELEMS * (int)sizeof(T) / 1024 / (gdr::NT / 64);
+  static constexpr int INS_PHI = R::UV * (int)sizeof(T) / 1024 / (gdr::NT / 64);
+  static_assert(R::ELEMS * sizeof(T) % (1024 * (gdr::NT / 64)) == 0 && R::UV * sizeof(T) % (1024 * (gdr::NT / 64)) == 0,
+                "every wave copies the same number of KiB");
+  static_assert(bytes <= 160 * 1024 && INS_PSI < 64, "fits LDS and the vmcnt counter");
 };
 
-// The chunk step S <- gamma_C S + Kt (Uv - W S) is affine in S, so a run of chunks maps a
-// start state S to Phi S + Psi. A long sequence is cut into ws.P segments: k_gdr_scan_seg runs
-// every segment at once from the start states I (for Phi, without Uv) and 0 (for Psi), and
-// k_gdr_combine_seg then applies the segments in order, S <- Phi_g S + Psi_g. With one segment
-// k_gdr_scan reads and writes S directly.
-template <typename T, int DK, int DV>
-__global__ __launch_bounds__(gdr::NT) void k_gdr_scan(float* __restrict__ S, int Hv, int N,
-                                                      GdrWs ws) {
-  using namespace gdr;
-  typedef typename Frag8<T>::type F;
-  typedef ScanLds<T, DK> L;
-  extern __shared__ __align__(16) unsigned char smem[];
-  T* Ssh = (T*)(smem + L::ssh);  // state slice, [column][dk]: B operand of U = Uv - W S
-  T* Ush = (T*)(smem + L::ush);  // U slice, [column][token]: B operand of S += Kt U
-  constexpr int SP = DK + PAD, UP = C + PAD;
-  const int sl = blockIdx.x * 32, hv = blockIdx.y, b = blockIdx.z;
-  const int NC = (N + C - 1) / C;
-  const int64_t seq = (int64_t)b * Hv + hv;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int h = lane >> 5, rr = lane & 31;
-  const bool holds = wave * 32 < DK;  // this wave keeps state rows [32 wave, 32 wave + 32)
-  const bool makes_u = wave * 32 < C;  // this wave computes U rows [32 wave, 32 wave + 32)
-  float* Sg = S + seq * DK * DV;
-
-  f32x16 st = {};
-  if (holds) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) st[i] = Sg[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + sl + rr];
-  }
-  // Operands of one chunk, loaded one chunk ahead: W rows (A operand of U = Uv - W S), the Uv
-  // entries of this lane's accumulator positions, Kt rows (A operand of S += Kt U) and gamma_C.
-  F wf[DK / 16], kf[C / 16];
-  T uv[16];
-  float gcn = 1.f;
-  auto fetch = [&](int c) {
-    const int64_t cid = seq * NC + c;
-    gcn = ws.gc[cid];
-    if (makes_u) {
-      const T* W = ws.w<T>(cid, DK) + (int64_t)(wave * 32 + rr) * DK;
-#pragma unroll
-      for (int ks = 0; ks < DK / 16; ++ks) wf[ks] = *(const F*)(W + ks * 16 + h * 8);
-      const T* Uv = ws.uv<T>(cid, DV);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) uv[i] = Uv[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + sl + rr];
-    }
-    if (holds) {
-      const T* Kt = ws.kt<T>(cid, DK) + (int64_t)(wave * 32 + rr) * C;
-#pragma unroll
-      for (int ks = 0; ks < C / 16; ++ks) kf[ks] = *(const F*)(Kt + ks * 16 + h * 8);
-    }
-  };
-  fetch(0);
-  for (int c = 0; c < NC; ++c) {
-    F wnow[DK / 16], know[C / 16];
-    T unow[16];
-#pragma unroll
-    for (int q = 0; q < DK / 16; ++q) wnow[q] = wf[q];
-#pragma unroll
-    for (int q = 0; q < C / 16; ++q) know[q] = kf[q];
-#pragma unroll
-    for (int q = 0; q < 16; ++q) unow[q] = uv[q];
-    const float gc = gcn;
-    if (c + 1 < NC) fetch(c + 1);
-    // (a) publish the state slice in the call dtype
-    if (holds) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Ssh[rr * SP + wave * 32 + acc_row(lane, i)] = from_f32<T>(st[i]);
-    }
-    __syncthreads();
-    // (b) U = Uv - W S for this slice (two independent MFMA chains)
-    if (makes_u) {
-      f32x16 acc0 = {}, acc1 = {};
-#pragma unroll
-      for (int ks = 0; ks < DK / 16; ks += 2) {
-        mfma_k16(acc0, wnow[ks], *(const F*)(Ssh + rr * SP + ks * 16 + h * 8));
-        mfma_k16(acc1, wnow[ks + 1], *(const F*)(Ssh + rr * SP + (ks + 1) * 16 + h * 8));
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        Ush[rr * UP + wave * 32 + acc_row(lane, i)] =
-            from_f32<T>(to_f32(unow[i]) - (acc0[i] + acc1[i]));
-    }
-    __syncthreads();
-    // (c) S = gamma_C S + Kt U
-    if (holds) {
-      f32x16 p0 = {}, p1 = {};
-#pragma unroll
-      for (int ks = 0; ks < C / 16; ks += 2) {
-        mfma_k16(p0, know[ks], *(const F*)(Ush + rr * UP + ks * 16 + h * 8));
-        mfma_k16(p1, know[ks + 1], *(const F*)(Ush + rr * UP + (ks + 1) * 16 + h * 8));
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) st[i] = st[i] * gc + (p0[i] + p1[i]);
-    }
-  }
-  if (holds) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) Sg[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + sl + rr] = st[i];
-  }
+// Copies one chunk record (a multiple of 1 KiB) into LDS, 1 KiB per wave instruction, waves
+// taking every fourth KiB. Straight into LDS: nothing passes through registers.
+__device__ __forceinline__ void gdr_copy_record(const void* src, int bytes, unsigned char* dst, int wave, int nins) {
+  const auto rs = buffer_rsrc(src, bytes);
+  const int lane = threadIdx.x & 63;
+  for (int blk = wave; blk < nins; blk += gdr::NT / 64)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + blk * 1024), 16, lane * 16, blk * 1024, 0, 0);
 }
 
-// Two-level scan kernels for dk = dv = 128: one block owns all 128 columns of its state (the
-// Phi block or the Psi block of a segment, or the state in the combine), so every chunk's W and
-// Kt are read once per block. Wave w keeps state rows [32 w, 32 w + 32) of all four column
-// tiles; the U tiles (2 token tiles x 4 column tiles) are shared out two per wave.
-template <typename T>
-struct FullLds {
-  static constexpr int C = gdr::C, P = gdr::PAD;
-  static constexpr size_t ssh = 0;                                        // T[128][128+P]
-  static constexpr size_t ush = ssh + (size_t)128 * (128 + P) * sizeof(T);  // T[128][C+P]
-  static constexpr size_t bytes = ush + (size_t)128 * (C + P) * sizeof(T);
-};
+// Column blocks of 128 state columns.
+constexpr int gdr_xblocks(int cols) { return (cols + 127) / 128; }
 
-template <typename T>
-__global__ __launch_bounds__(gdr::NT) void k_gdr_scan_seg(int Hv, int N, GdrWs ws) {
+// The chunks of one segment (the whole sequence when ws.P == 1) in order for one (sequence,
+// value head): grid (column blocks, Hv, B * P). With P > 1 the first gdr_xblocks(DK) column
+// blocks carry the columns of Phi, the others those of Psi. Each wave owns 32 columns.
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(gdr::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gdr_chain(float* __restrict__ S, const float* __restrict__ gcs, int Hv, int N, GdrWs ws) {
   using namespace gdr;
-  typedef typename Frag8<T>::type F;
-  typedef FullLds<T> L;
-  constexpr int DK = 128, DV = 128, NCT = 4;  // column tiles of 32
+  typedef GdrRec<T, DK, DV> R;
+  typedef ChainLds<T, DK, DV> L;
+  constexpr int NKT = DK / 32, XPHI = gdr_xblocks(DK);
   extern __shared__ __align__(16) unsigned char smem[];
-  T* Ssh = (T*)(smem + L::ssh);  // [column][dk]
-  T* Ush = (T*)(smem + L::ush);  // [column][token]
-  constexpr int SP = DK + PAD, UP = C + PAD;
   const int P = ws.P;
-  const bool phi = blockIdx.x == 0;
   const int hv = blockIdx.y, b = blockIdx.z / P, seg = blockIdx.z - b * P;
+  const bool phi = P > 1 && (int)blockIdx.x < XPHI;
+  if (phi && seg == 0) return;  // segment 0 starts from S itself: no transition matrix needed
+  const int xb = P > 1 && !phi ? blockIdx.x - XPHI : blockIdx.x;
+  const int ncols = phi ? DK : DV;
   const int NC = (N + C - 1) / C;
   const int c_begin = seg * ws.cps, c_end = min(NC, c_begin + ws.cps);
   const int64_t seq = (int64_t)b * Hv + hv;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_index();
   const int h = lane >> 5, rr = lane & 31;
-  const int ut = wave & 1;        // token tile of this wave's U tiles
-  const int uc0 = wave >> 1;      // its U column tiles: uc0 and uc0 + 2
+  const int n0 = xb * 128 + wave * 32;  // first column of this wave
+  const bool active = n0 < ncols;
+  const bool from_s = P == 1 || (!phi && seg == 0);
+  const bool uses_uv = !phi;
+  const int copy_bytes = (uses_uv ? R::ELEMS : R::UV) * (int)sizeof(T);
+  const int nins = copy_bytes / 1024;  // 1 KiB per wave instruction (64 lanes x 16 bytes)
 
-  f32x16 st[NCT];
+  f32x16 st[NKT];
 #pragma unroll
-  for (int j = 0; j < NCT; ++j)
+  for (int kt = 0; kt < NKT; ++kt) st[kt] = f32x16{};
+  if (active) {
+    if (from_s) {
+      const float* Sg = S + seq * DK * DV + n0 + rr;
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      st[j][i] = (phi && wave * 32 + acc_row(lane, i) == j * 32 + rr) ? 1.f : 0.f;
-
-  F wf[DK / 16], kf[C / 16];
-  T uv[2][16];
-  float gcn = 1.f;
-  auto fetch = [&](int c) {
-    const int64_t cid = seq * NC + c;
-    gcn = ws.gc[cid];
-    const T* W = ws.w<T>(cid, DK) + (int64_t)(ut * 32 + rr) * DK;
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-    for (int ks = 0; ks < DK / 16; ++ks) wf[ks] = *(const F*)(W + ks * 16 + h * 8);
-    const T* Kt = ws.kt<T>(cid, DK) + (int64_t)(wave * 32 + rr) * C;
+        for (int i = 0; i < 16; ++i) st[kt][i] = Sg[(int64_t)(kt * 32 + acc_row(lane, i)) * DV];
+    } else if (phi) {
 #pragma unroll
-    for (int ks = 0; ks < C / 16; ++ks) kf[ks] = *(const F*)(Kt + ks * 16 + h * 8);
-    if (!phi) {
-      const T* Uv = ws.uv<T>(cid, DV) + (int64_t)(ut * 32) * DV + uc0 * 32 + rr;
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) uv[q][i] = Uv[(int64_t)acc_row(lane, i) * DV + q * 64];
-    }
-  };
-#pragma unroll
-  for (int q = 0; q < 2; ++q)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) uv[q][i] = from_f32<T>(0.f);
-  if (c_begin < c_end) fetch(c_begin);
-  for (int c = c_begin; c < c_end; ++c) {
-    F wnow[DK / 16], know[C / 16];
-    T unow[2][16];
-#pragma unroll
-    for (int q = 0; q < DK / 16; ++q) wnow[q] = wf[q];
-#pragma unroll
-    for (int q = 0; q < C / 16; ++q) know[q] = kf[q];
-#pragma unroll
-    for (int q = 0; q < 2; ++q)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) unow[q][i] = uv[q][i];
-    const float gc = gcn;
-    if (c + 1 < c_end) fetch(c + 1);
-    // (a) publish the state in the call dtype
-#pragma unroll
-    for (int j = 0; j < NCT; ++j)
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        Ssh[(j * 32 + rr) * SP + wave * 32 + acc_row(lane, i)] = from_f32<T>(st[j][i]);
-    __syncthreads();
-    // (b) U = Uv - W S: this wave's two tiles (token tile ut, column tiles uc0, uc0 + 2)
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int uc = uc0 + 2 * q;
-      f32x16 a0 = {}, a1 = {};
-#pragma unroll
-      for (int ks = 0; ks < DK / 16; ks += 2) {
-        mfma_k16(a0, wnow[ks], *(const F*)(Ssh + (uc * 32 + rr) * SP + ks * 16 + h * 8));
-        mfma_k16(a1, wnow[ks + 1], *(const F*)(Ssh + (uc * 32 + rr) * SP + (ks + 1) * 16 + h * 8));
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        Ush[(uc * 32 + rr) * UP + ut * 32 + acc_row(lane, i)] =
-            from_f32<T>(to_f32(unow[q][i]) - (a0[i] + a1[i]));
-      }
-    }
-    __syncthreads();
-    // (c) S = gamma_C S + Kt U for all four column tiles of this wave's rows
-#pragma unroll
-    for (int j = 0; j < NCT; ++j) {
-      f32x16 p0 = {}, p1 = {};
-#pragma unroll
-      for (int ks = 0; ks < C / 16; ks += 2) {
-        mfma_k16(p0, know[ks], *(const F*)(Ush + (j * 32 + rr) * UP + ks * 16 + h * 8));
-        mfma_k16(p1, know[ks + 1], *(const F*)(Ush + (j * 32 + rr) * UP + (ks + 1) * 16 + h * 8));
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) st[j][i] = st[j][i] * gc + (p0[i] + p1[i]);
+        for (int i = 0; i < 16; ++i) st[kt][i] = kt * 32 + acc_row(lane, i) == n0 + rr ? 1.f : 0.f;
     }
   }
-  float* out = phi ? ws.phi + (seq * P + seg) * DK * DK : ws.psi + (seq * P + seg) * DK * DV;
+
+  auto issue = [&](int c, int stage) {
+    gdr_copy_record(ws.rec<T>(seq * NC + c), copy_bytes, smem + (size_t)stage * R::ELEMS * sizeof(T), wave, nins);
+  };
+
+  issue(c_begin, 0);
+  if (L::NS == 3 && c_begin + 1 < c_end) issue(c_begin + 1, 1);
+  int stage = 0;
+  for (int c = c_begin; c < c_end; ++c) {
+    const float gc = gcs[seq * NC + c];
+    // This wave's copies of chunk c have landed (those of chunk c + 1, issued after them, may
+    // still be in flight); the barrier makes that true of every wave and ends every wave's reads
+    // of the buffer that chunk c + 2 goes to.
+    if (L::NS == 3 && c + 1 < c_end) {
+      if (uses_uv)
+        pipe_sync<waitcnt_imm(L::INS_PSI, 0)>();
+      else
+        pipe_sync<waitcnt_imm(L::INS_PHI, 0)>();
+    } else {
+      pipe_sync<waitcnt_imm(0, 0)>();
+    }
+    if (L::NS == 3 && c + 2 < c_end) issue(c + 2, stage == 0 ? 2 : stage - 1);
+    if (active) {
+      typedef typename Frag8<T>::type F;
+      const T* Wn = (const T*)(smem + (size_t)stage * R::ELEMS * sizeof(T));
+      const T* Kt = Wn + R::KT;
+      const T* UvT = Wn + R::UV;
+      // Every fragment of the step is read up front (one block per CU leaves the registers
+      // for it), so that LDS latency is paid once per phase, not once per MFMA.
+      F wf[2][NKT][2], uf[2][2];
 #pragma unroll
-  for (int j = 0; j < NCT; ++j)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) out[(int64_t)(wave * 32 + acc_row(lane, i)) * 128 + j * 32 + rr] = st[j][i];
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt) wf[tt][kt][q] = frag_get<T, DK>(Wn, tt * 32 + rr, kt * 4 + 2 * q + h);
+      // (read in Phi blocks too, where the buffer's Uv part is stale: the values are not used)
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) uf[tt][q] = frag_get<T, C>(UvT, n0 + rr, tt * 4 + 2 * q + h);
+      // U = Uv - W S for the two token tiles (the record holds -W); S enters rounded to T
+      F sb[NKT][2];
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        sb[kt][0] = acc_frag<T>(st[kt], 0);
+        sb[kt][1] = acc_frag<T>(st[kt], 1);
+      }
+      f32x16 u[2];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) u[tt][8 * q + e] = uses_uv ? to_f32(uf[tt][q][e]) : 0.f;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt) mfma_k16(u[tt], wf[tt][kt][q], sb[kt][q]);
+      // S = gamma_C S + Kt U
+      F kf[NKT][2][2];
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int q = 0; q < 2; ++q) kf[kt][tt][q] = frag_get<T, C>(Kt, kt * 32 + rr, tt * 4 + 2 * q + h);
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) st[kt] *= gc;
+      F ub[2][2];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        ub[tt][0] = acc_frag<T>(u[tt], 0);
+        ub[tt][1] = acc_frag<T>(u[tt], 1);
+      }
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt) mfma_k16(st[kt], kf[kt][tt][q], ub[tt][q]);
+      // Schedule: the W and Uv reads first, then the U products with the Kt reads between them
+      // (they land while the products run), then the state products.
+      if constexpr (sizeof(T) == 2) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 4 * NKT + 4, 0);
+#pragma unroll
+        for (int i = 0; i < 4 * NKT; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * NKT, 0);
+      }
+    }
+    if (L::NS == 1 && c + 1 < c_end) {
+      __syncthreads();
+      issue(c + 1, 0);
+    }
+    stage = L::NS == 3 ? (stage == 2 ? 0 : stage + 1) : 0;
+  }
+  if (!active) return;
+  float* out;
+  int ld;
+  if (P == 1) {
+    out = S + seq * DK * DV;
+    ld = DV;
+  } else if (phi) {
+    out = ws.phi + (seq * P + seg) * DK * DK;
+    ld = DK;
+  } else {
+    out = ws.psi + (seq * P + seg) * DK * DV;
+    ld = DV;
+  }
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) out[(int64_t)(kt * 32 + acc_row(lane, i)) * ld + n0 + rr] = st[kt][i];
 }
 
-// S <- Phi_g S + Psi_g for g = 0 .. P-1, one block per (sequence, value head), all 128 columns.
-template <typename T>
-__global__ __launch_bounds__(gdr::NT) void k_gdr_combine_seg(float* __restrict__ S, int Hv, GdrWs ws) {
-  using namespace gdr;
+// S <- Phi_g S + Psi_g for g = 1 .. P-1, from S = Psi_0; grid (column blocks, Hv, B), 32 state
+// columns per wave. Phi_g is read as the A operand in the k order of the state's accumulators
+// (two runs of four fp32 per lane half) and rounded to the call dtype, as the chunk steps round
+// their operands.
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(gdr::NT) void k_gdr_merge(float* __restrict__ S, int Hv, GdrWs ws) {
   typedef typename Frag8<T>::type F;
-  typedef FullLds<T> L;
-  constexpr int DK = 128, DV = 128, NCT = 4;
-  extern __shared__ __align__(16) unsigned char smem[];
-  T* Ssh = (T*)(smem + L::ssh);
-  constexpr int SP = DK + PAD;
+  constexpr int NKT = DK / 32;
   const int P = ws.P;
   const int hv = blockIdx.y, b = blockIdx.z;
   const int64_t seq = (int64_t)b * Hv + hv;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_index();
   const int h = lane >> 5, rr = lane & 31;
-  float* Sg = S + seq * DK * DV;
-  f32x16 st[NCT];
+  const int n0 = blockIdx.x * 128 + wave * 32;
+  if (n0 >= DV) return;
+  f32x16 st[NKT];
+  const float* Ps = ws.psi + seq * P * DK * DV + n0 + rr;
 #pragma unroll
-  for (int j = 0; j < NCT; ++j)
+  for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) st[j][i] = Sg[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + j * 32 + rr];
-  F af[DK / 16];
-  auto fetch = [&](int g) {
-    const float* Phi = ws.phi + (seq * P + g) * DK * DK + (int64_t)(wave * 32 + rr) * DK;
+    for (int i = 0; i < 16; ++i) st[kt][i] = Ps[(int64_t)(kt * 32 + acc_row(lane, i)) * DV];
+  for (int g = 1; g < P; ++g) {
+    F sb[NKT][2];
 #pragma unroll
-    for (int ks = 0; ks < DK / 16; ++ks) {
-      const f32x4 lo = *(const f32x4*)(Phi + ks * 16 + h * 8);
-      const f32x4 hi = *(const f32x4*)(Phi + ks * 16 + h * 8 + 4);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        af[ks][e] = from_f32<T>(lo[e]);
-        af[ks][e + 4] = from_f32<T>(hi[e]);
-      }
+    for (int kt = 0; kt < NKT; ++kt) {
+      sb[kt][0] = acc_frag<T>(st[kt], 0);
+      sb[kt][1] = acc_frag<T>(st[kt], 1);
     }
-  };
-  fetch(0);
-  for (int g = 0; g < P; ++g) {
-    F anow[DK / 16];
+    const float* Pg = ws.psi + (seq * P + g) * DK * DV + n0 + rr;
 #pragma unroll
-    for (int q = 0; q < DK / 16; ++q) anow[q] = af[q];
-    if (g + 1 < P) fetch(g + 1);
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-    for (int j = 0; j < NCT; ++j)
+      for (int i = 0; i < 16; ++i) st[kt][i] = Pg[(int64_t)(kt * 32 + acc_row(lane, i)) * DV];
+    const float* Phi = ws.phi + (seq * P + g) * DK * DK;
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        Ssh[(j * 32 + rr) * SP + wave * 32 + acc_row(lane, i)] = from_f32<T>(st[j][i]);
-    __syncthreads();
-    const float* Psi = ws.psi + (seq * P + g) * DK * DV;
+    for (int kt = 0; kt < NKT; ++kt) {
+      const float* row = Phi + (int64_t)(kt * 32 + rr) * DK + 4 * h;
 #pragma unroll
-    for (int j = 0; j < NCT; ++j) {
-      f32x16 p0 = {}, p1 = {};
+      for (int k2 = 0; k2 < NKT; ++k2)
 #pragma unroll
-      for (int ks = 0; ks < DK / 16; ks += 2) {
-        mfma_k16(p0, anow[ks], *(const F*)(Ssh + (j * 32 + rr) * SP + ks * 16 + h * 8));
-        mfma_k16(p1, anow[ks + 1], *(const F*)(Ssh + (j * 32 + rr) * SP + (ks + 1) * 16 + h * 8));
-      }
+        for (int q = 0; q < 2; ++q) {
+          const f32x4 lo = *(const f32x4*)(row + k2 * 32 + 16 * q);
+          const f32x4 hi = *(const f32x4*)(row + k2 * 32 + 16 * q + 8);
+          F a;
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        st[j][i] = (p0[i] + p1[i]) + Psi[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + j * 32 + rr];
+          for (int e = 0; e < 4; ++e) {
+            a[e] = from_f32<T>(lo[e]);
+            a[e + 4] = from_f32<T>(hi[e]);
+          }
+          mfma_k16(st[kt], a, sb[k2][q]);
+        }
     }
-    __syncthreads();  // every wave is done reading Ssh before the next step rewrites it
   }
+  float* Sg = S + seq * DK * DV + n0 + rr;
 #pragma unroll
-  for (int j = 0; j < NCT; ++j)
+  for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) Sg[(int64_t)(wave * 32 + acc_row(lane, i)) * DV + j * 32 + rr] = st[j][i];
+    for (int i = 0; i < 16; ++i) Sg[(int64_t)(kt * 32 + acc_row(lane, i)) * DV] = st[kt][i];
 }
 
 template <typename K>
@@ -580,14 +614,10 @@ static hipError_t gdr_launch(const void* k, const void* v, const float* alpha, c
                              float* S, int B, int Hk, int Hv, int N, GdrWs ws, hipStream_t s,
                              const LaunchEvents& ev) {
   typedef GdrLds<T, DK, DV> LP;
-  typedef ScanLds<T, DK> LS;
+  typedef ChainLds<T, DK, DV> LC;
   static bool once = [] {
     allow_lds_bytes(k_gdr_prep<T, DK, DV>, LP::bytes);
-    allow_lds_bytes(k_gdr_scan<T, DK, DV>, LS::bytes);
-    if constexpr (DK == 128 && DV == 128) {
-      allow_lds_bytes(k_gdr_scan_seg<T>, FullLds<T>::bytes);
-      allow_lds_bytes(k_gdr_combine_seg<T>, FullLds<T>::bytes);
-    }
+    allow_lds_bytes(k_gdr_chain<T, DK, DV>, LC::bytes);
     return true;
   }();
   (void)once;
@@ -599,41 +629,46 @@ static hipError_t gdr_launch(const void* k, const void* v, const float* alpha, c
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   record(ev.gdr_scan[0], s);
+  const int xblocks = ws.P > 1 ? gdr_xblocks(DK) + gdr_xblocks(DV) : gdr_xblocks(DV);
+  k_gdr_chain<T, DK, DV><<<dim3(xblocks, Hv, B * ws.P), gdr::NT, LC::bytes, s>>>(S, ws.gc, Hv, N, ws);
   if (ws.P > 1) {
-    if constexpr (DK == 128 && DV == 128) {
-      k_gdr_scan_seg<T><<<dim3(2, Hv, B * ws.P), gdr::NT, FullLds<T>::bytes, s>>>(Hv, N, ws);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
-      k_gdr_combine_seg<T><<<dim3(1, Hv, B), gdr::NT, FullLds<T>::bytes, s>>>(S, Hv, ws);
-    } else {
-      return hipErrorInvalidValue;  // segments are only planned for dk = dv = 128
-    }
-  } else {
-    k_gdr_scan<T, DK, DV><<<dim3(DV / 32, Hv, B), gdr::NT, LS::bytes, s>>>(S, Hv, N, ws);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_gdr_merge<T, DK, DV><<<dim3(gdr_xblocks(DV), Hv, B), gdr::NT, 0, s>>>(S, Hv, ws);
   }
   record(ev.gdr_scan[1], s);
   return hipGetLastError();
 }
 
-// Segments of the two-level scan, from a latency model of the two schedules (times per chunk
-// step measured on MI355X at dk = dv = 128): the plain scan runs every chunk in order at about
-// 1.5 us a step with DV / 32 small blocks per sequence; the segmented scan runs ceil(NC / P)
-// steps at about 3.4 us, in as many rounds as its 2 B Hv P one-per-CU blocks need, and the
-// combine adds P steps of about 3.7 us. P = 1 selects the plain scan. The scan's grid dimension
-// B * P stays within 65535.
-static void gdr_segments(int NC, int B, int Hv, int dk, int dv, int& P, int& cps) {
+// Segments of the two-level scan, from a model of k_gdr_chain fitted on MI355X: one block per
+// CU, a chunk step bounded by the record stream of one CU (about 35 GB/s, 1.4 us for a 48 KiB
+// record) or by its MFMA chain (about 0.6 us), the records of all offset blocks together by HBM
+// (about 4.4 TB/s), and about 3 us per segment in k_gdr_merge. The transition-matrix blocks
+// read the same records as the offset blocks of their segment, at about the same time; counting
+// their bytes in the HBM term as well made the model choose fewer segments than the measured
+// optimum (4 for 256 chunks x 32 heads). P = 1 runs the whole sequence in order. The grid
+// dimension B * P stays within 65535.
+static void gdr_segments(int NC, int B, int Hv, int dk, int dv, int esize, int& P, int& cps) {
+  const double cus = 256.0, merge_us = 3.0, cu_bytes_per_us = 35.0e3, hbm_bytes_per_us = 4.4e6;
+  const double seqs = (double)B * Hv;
+  const double rec = 64.0 * (2 * dk + dv) * esize;
+  const double step_us = std::max(0.6, rec / cu_bytes_per_us);
+  const int xk = gdr_xblocks(dk), xv = gdr_xblocks(dv);
+  auto cost = [&](int p, int c) {
+    const double blocks = seqs * (p > 1 ? (double)p * (xk + xv) - xk : xv);
+    const double rounds = std::ceil(blocks / cus);
+    const double bytes = seqs * NC * rec * xv;
+    const double t = std::max(rounds * c * step_us, bytes / hbm_bytes_per_us);
+    return t + (p > 1 ? (p - 1) * merge_us * std::ceil(seqs * xv / cus) : 0.0);
+  };
   P = 1;
   cps = NC;
-  if (dk != 128 || dv != 128 || NC < 16) return;
-  const double cus = 256.0;
-  const double plain_rounds = std::ceil(B * (double)Hv * (dv / 32) / (cus * 8));
-  double best = plain_rounds * NC * 1.5;
+  double best = cost(1, NC);
   const int pmax = std::min(64, std::min(NC / 2, 65535 / B));
   for (int p = 2; p <= pmax; ++p) {
     const int c = (NC + p - 1) / p;
     const int pp = (NC + c - 1) / c;
-    const double rounds = std::ceil(2.0 * B * Hv * pp / cus);
-    const double t = rounds * c * 3.4 + pp * 3.7 * std::ceil(B * (double)Hv / cus);
+    const double t = cost(pp, c);
     if (t < best) {
       best = t;
       P = pp;
@@ -648,12 +683,12 @@ GdrWs gdr_layout(void* base, int B, int Hv, int N, int dk, int dv, int dtype) {
   const int64_t chunks = (int64_t)B * Hv * NC;
   auto al = [](size_t x) { return (x + 255) / 256 * 256; };
   GdrWs w{};
-  gdr_segments(NC, B, Hv, dk, dv, w.P, w.cps);
+  gdr_segments(NC, B, Hv, dk, dv, (int)e, w.P, w.cps);
+  w.rec_elems = gdr::C * (2 * dk + dv);
   char* p = (char*)base;
   size_t o = 0;
-  w.w_ = p ? p + o : nullptr;   o += al((size_t)chunks * gdr::C * dk * e);
-  w.uv_ = p ? p + o : nullptr;  o += al((size_t)chunks * gdr::C * dv * e);
-  w.kt_ = p ? p + o : nullptr;  o += al((size_t)chunks * gdr::C * dk * e);
+  w.rec_ = p ? p + o : nullptr;
+  o += al((size_t)chunks * w.rec_elems * e);
   w.gc = p ? (float*)(p + o) : nullptr;
   o += al((size_t)chunks * 4);
   const size_t segs = w.P > 1 ? (size_t)B * Hv * w.P : 0;

@@ -9,25 +9,21 @@
 
 namespace dv {
 
-// Workspace of the chunked delta rule: per (sequence, value head, chunk of 64 tokens) the
-// products W [64][dk], Uv [64][dv], Kt [dk][64] in the call dtype and gamma_C (fp32), and per
-// segment of the two-level scan the affine map (Phi, Psi) in fp32.
+// Workspace of the chunked delta rule: per (sequence, value head, chunk of 64 tokens) one
+// record of -W [64][dk], Kt [dk][64] and Uv^T [dv][64] in the call dtype (in the fragment order
+// of the chunk kernels) and gamma_C (fp32), and per segment of the two-level scan the affine
+// map (Phi, Psi) in fp32.
 struct GdrWs {
-  void* w_;
-  void* uv_;
-  void* kt_;
+  void* rec_;
   float* gc;
-  float* phi;  // per segment: the linear part Phi [dk][dk] of the segment's affine map
-  float* psi;  // per segment: the state Psi [dk][dv] it reaches from a zero start
-  int P;       // segments of the two-level scan (1: a single in-order scan)
-  int cps;     // chunks per segment
+  float* phi;     // per segment: the linear part Phi [dk][dk] of the segment's affine map
+  float* psi;     // per segment: the state Psi [dk][dv] it reaches (segment 0: from S)
+  int P;          // segments of the two-level scan (1: a single in-order scan)
+  int cps;        // chunks per segment
+  int rec_elems;  // elements per chunk record, 64 (2 dk + dv)
   size_t bytes;
   template <typename T>
-  __host__ __device__ T* w(int64_t chunk, int dk) const { return (T*)w_ + chunk * 64 * dk; }
-  template <typename T>
-  __host__ __device__ T* uv(int64_t chunk, int dv) const { return (T*)uv_ + chunk * 64 * dv; }
-  template <typename T>
-  __host__ __device__ T* kt(int64_t chunk, int dk) const { return (T*)kt_ + chunk * 64 * dk; }
+  __host__ __device__ T* rec(int64_t chunk) const { return (T*)rec_ + chunk * rec_elems; }
 };
 
 // Layout of the workspace at base (sizes only when base is null).
