@@ -113,27 +113,67 @@ struct GdrRec {
   static constexpr int KT = C * DK, UV = 2 * C * DK, ELEMS = C * (2 * DK + DV);
 };
 
-// LDS layout of k_gdr_prep (byte offsets). For bf16, T diag(beta) and T diag(beta gamma)
-// (unpadded rows) reuse the bytes of A, which is dead once A21 T11 is formed; the block then
-// stays under 80 KiB so that two share a CU.
+// The chunk's K and V transposed in LDS ([channel][token], 64 tokens a row): 16-byte chunks of a
+// row XOR-swizzled by the row, so that the 16 rows one fragment load touches fall in distinct
+// bank groups without padding.
+template <typename T>
+__device__ __forceinline__ int vk_off(int n, int s) {
+  constexpr int EPC = 16 / (int)sizeof(T), CPR = gdr::C / EPC;
+  const int key = CPR >= 16 ? (n & 15) : ((n >> 1) & 7);
+  return n * gdr::C + (((s / EPC) ^ key) * EPC) + s % EPC;
+}
+
+// 8 consecutive tokens s0 .. s0 + 7 (s0 a multiple of 8) of row n.
+template <typename T>
+__device__ __forceinline__ typename Frag8<T>::type vk_frag(const T* m, int n, int s0) {
+  typedef typename Frag8<T>::type F;
+  if constexpr (sizeof(T) == 2) {
+    return *(const F*)(m + vk_off<T>(n, s0));
+  } else {
+    const f32x4 lo = *(const f32x4*)(m + vk_off<T>(n, s0));
+    const f32x4 hi = *(const f32x4*)(m + vk_off<T>(n, s0 + 4));
+    return F{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  }
+}
+
+// LDS layout of k_gdr_prep (byte offsets). M holds A and is turned into T = (I + A)^-1 in place;
+// the bf16 block stays under 53 KiB so that three share a CU.
 template <typename T, int DK, int DV>
 struct GdrLds {
-  static constexpr int C = gdr::C, P = gdr::PAD;
-  static constexpr bool kReuse = sizeof(T) == 2;
-  static constexpr int TWP = kReuse ? C : C + P;                          // pitch of Tu, Tw
-  static constexpr size_t g = 0;                                          // float[C]  g_t
-  static constexpr size_t beta = g + C * 4;                               // float[C]
-  static constexpr size_t am = beta + C * 4;                              // float[C][C]  A
-  static constexpr size_t tf = am + (size_t)C * C * 4;                    // float[C][C+1] T (fp32)
-  static constexpr size_t xb = tf + (size_t)C * (C + 1) * 4;              // float[32][33] A21 T11
-  static constexpr size_t vt = xb + (size_t)32 * 33 * 4;                  // T[DV][C+P] V^T
-  static constexpr size_t kt = vt + (size_t)DV * (C + P) * sizeof(T);     // T[DK][C+P] K^T
-  static constexpr size_t end = kt + (size_t)DK * (C + P) * sizeof(T);
-  static constexpr size_t tu = kReuse ? am : end;                         // T[C][TWP] T diag(beta)
-  static constexpr size_t tw = tu + (size_t)C * TWP * sizeof(T);          // T[C][TWP] T diag(beta gamma)
-  static constexpr size_t bytes = kReuse ? end : tw + (size_t)C * TWP * sizeof(T);
-  static_assert(!kReuse || 2 * C * TWP * sizeof(T) <= (size_t)C * C * 4, "Tu and Tw fit in A");
+  static constexpr int C = gdr::C;
+  static constexpr int MP = C + 4;                                 // fp32 pitch of M (bank spread)
+  static constexpr size_t g = 0;                                   // float[C]  g_t
+  static constexpr size_t beta = g + C * 4;                        // float[C]  beta_t
+  static constexpr size_t bg = beta + C * 4;                       // float[C]  beta_t gamma_t
+  static constexpr size_t m = bg + C * 4;                          // float[C][MP]
+  static constexpr size_t vt = m + (size_t)C * MP * 4;             // T[DV][C]  V^T
+  static constexpr size_t kt = vt + (size_t)DV * C * sizeof(T);    // T[DK][C]  K^T
+  static constexpr size_t bytes = kt + (size_t)DK * C * sizeof(T);
 };
+
+// D[16x16] += A[16x4] B[4x16] in fp32; lane l gives A[l % 16][l / 16] and B[l / 16][l % 16] and
+// holds D[4 (l / 16) + r][l % 16] in item r.
+__device__ __forceinline__ void mfma16x4(f32x4& d, float a, float b) {
+  d = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, d, 0, 0, 0);
+}
+
+// out[16x16] = X[16 x 4 nk] Y[4 nk x 16] for fp32 matrices in M (pitch MP); X rows from xr, its
+// columns from xc; Y rows from yr, its columns from yc; k runs over 4 k0 .. 4 (k0 + nk) - 1.
+template <int MP>
+__device__ __forceinline__ f32x4 mm16(const float* M, int xr, int xc, int yr, int yc, int k0, int nk) {
+  const int lane = threadIdx.x & 63, i = lane & 15, kk = lane >> 4;
+  f32x4 d = {};
+  for (int ks = k0; ks < k0 + nk; ++ks)
+    mfma16x4(d, M[(xr + i) * MP + xc + 4 * ks + kk], M[(yr + 4 * ks + kk) * MP + yc + i]);
+  return d;
+}
+
+template <int MP>
+__device__ __forceinline__ void put16(float* M, int r0, int c0, f32x4 d, float sign) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) M[(r0 + 4 * (lane >> 4) + r) * MP + c0 + (lane & 15)] = sign * d[r];
+}
 
 template <typename T, int DK, int DV>
 __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
@@ -144,15 +184,14 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
   using namespace gdr;
   typedef GdrLds<T, DK, DV> L;
   typedef typename Frag8<T>::type F;
+  constexpr int MP = L::MP;
   extern __shared__ __align__(16) unsigned char smem[];
   float* g = (float*)(smem + L::g);
   float* bet = (float*)(smem + L::beta);
-  float* Am = (float*)(smem + L::am);
-  T* Tu = (T*)(smem + L::tu);
-  T* Tw = (T*)(smem + L::tw);
+  float* bgm = (float*)(smem + L::bg);
+  float* M = (float*)(smem + L::m);
   T* VT = (T*)(smem + L::vt);
   T* KT = (T*)(smem + L::kt);
-  constexpr int CP = C + PAD;
 
   const int c = blockIdx.x, hv = blockIdx.y, b = blockIdx.z;
   const int NC = (N + C - 1) / C;
@@ -162,7 +201,7 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
   const int64_t seq = (int64_t)b * Hv + hv;  // (sequence, value head)
   const T* kc = k + (((int64_t)b * Hk + hk) * N + t0) * DK;
   const T* vc = v + (seq * N + t0) * DV;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_index();
   const int h = lane >> 5, rr = lane & 31;
 
   // Every global load of the block is issued first, so their latencies overlap: the gates,
@@ -210,6 +249,7 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
     }
     g[lane] = x;
     bet[lane] = be;
+    bgm[lane] = be * __expf(x);
   }
   // 2. The chunk's K and V, transposed into LDS (B operands of the two products, and the rows
   //    of Kt).
@@ -217,18 +257,19 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
   for (int q = 0; q < VP; ++q) {
     const int idx = tid + q * NT, sidx = idx % C, n0 = (idx / C) * 8;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) VT[(n0 + e) * CP + sidx] = vpc[q][e];
+    for (int e = 0; e < 8; ++e) VT[vk_off<T>(n0 + e, sidx)] = vpc[q][e];
   }
 #pragma unroll
   for (int q = 0; q < KP; ++q) {
     const int idx = tid + q * NT, sidx = idx % C, n0 = (idx / C) * 8;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) KT[(n0 + e) * CP + sidx] = kpc[q][e];
+    for (int e = 0; e < 8; ++e) KT[vk_off<T>(n0 + e, sidx)] = kpc[q][e];
   }
   __syncthreads();
   const float gC = g[C - 1];
 
-  // 3. A[t][s] = beta_t exp(g_t - g_s) k_t.k_s for s < t (K K^T on MFMA, lower tiles only).
+  // 3. A[t][s] = beta_t exp(g_t - g_s) k_t.k_s for s < t (K K^T on MFMA, lower tiles only; the
+  //    upper right tile of M is never read as part of A or T).
   if (wave < 3) {
     f32x16 acc = {};
 #pragma unroll
@@ -236,31 +277,27 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int t = ti3 * 32 + acc_row(lane, i), sx = si3 * 32 + rr;
-      Am[t * C + sx] = sx < t ? bet[t] * __expf(g[t] - g[sx]) * acc[i] : 0.f;
+      M[t * MP + sx] = sx < t ? bet[t] * __expf(g[t] - g[sx]) * acc[i] : 0.f;
     }
-  } else {
-    for (int e = lane; e < 32 * 32; e += 64) Am[(e >> 5) * C + 32 + (e & 31)] = 0.f;
   }
   __syncthreads();
 
-  // 4. T = (I + A)^-1 for the unit lower-triangular I + A, as a 2 x 2 block triangle:
-  //      T11 = (I + A11)^-1, T22 = (I + A22)^-1, T21 = -T22 A21 T11.
-  //    Wave 0 inverts both diagonal blocks by forward substitution (lanes 0..31 the columns
-  //    of T11, lanes 32..63 those of T22; each column is zero above its diagonal, so all lanes
-  //    run the same unrolled loops with the column in registers and the rows of A read as LDS
-  //    broadcasts, summed in four chains). Meanwhile the other waves write
-  //    Kt = (diag(gamma_C / gamma) K)^T.
-  float* Tf = (float*)(smem + L::tf);
-  float* Xb = (float*)(smem + L::xb);
-  constexpr int TP = C + 1;
+  // 4. T = (I + A)^-1 for the unit lower-triangular I + A, in place, by 2 x 2 block recursion
+  //    over 16 x 16 blocks D_0..D_3 on the diagonal:
+  //      level 0: D_b = (I + A_bb)^-1 by forward substitution (wave 0: lane 16 b + j runs
+  //               column j of D_b, the column in registers, rows of A read as LDS broadcasts
+  //               and summed in four chains; each row is read before it is overwritten);
+  //      level 1: in each 32 x 32 block p, T_(2p+1)(2p) = -D_(2p+1) (A_(2p+1)(2p) D_(2p));
+  //      level 2: T21 = -T22 (A21 T11).
+  //    Products run on fp32 MFMA (16x16x4), their intermediates in the upper right 32 x 32 block
+  //    of M, which the chunk's products never read. Meanwhile waves 1..3 write Kt.
   if (wave == 0) {
-    const int half = lane >> 5;            // 0: block (1,1), 1: block (2,2)
-    const int j = lane & 31, o = half * 32;
-    float col[32];
+    const int o = (lane >> 4) * 16, j = lane & 15;
+    float col[16];
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
+    for (int i = 0; i < 16; ++i) {
       float x4[4] = {0.f, 0.f, 0.f, 0.f};
-      const float* arow = Am + (o + i) * C + o;
+      const float* arow = M + (o + i) * MP + o;
 #pragma unroll
       for (int s4 = 0; s4 < i; s4 += 4) {
         const f32x4 a4 = *(const f32x4*)(arow + s4);
@@ -270,8 +307,7 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
       }
       const float x = (x4[0] + x4[1]) + (x4[2] + x4[3]);
       col[i] = i < j ? 0.f : (i == j ? 1.f : x);
-      Tf[(o + i) * TP + o + j] = col[i];
-      if (half == 0) Tf[i * TP + 32 + j] = 0.f;  // upper-right block
+      M[(o + i) * MP + o + j] = col[i];
     }
   } else {
     // Kt in fragment order: logical positions 8 gq .. 8 gq + 7 of row n hold tokens
@@ -279,73 +315,81 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
     T* Kt = ws.rec<T>(seq * NC + c) + GdrRec<T, DK, DV>::KT;
     for (int idx = tid - 64; idx < DK * (C / 8); idx += NT - 64) {
       const int n = idx / (C / 8), gq = idx % (C / 8);
-      const int t0 = (gq >> 1) * 16 + (gq & 1) * 4;
+      const int tq = (gq >> 1) * 16 + (gq & 1) * 4;
       F y;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int t = t0 + (e >> 2) * 8 + (e & 3);
-        y[e] = from_f32<T>(__expf(gC - g[t]) * to_f32(KT[n * CP + t]));
+        const int t = tq + (e >> 2) * 8 + (e & 3);
+        y[e] = from_f32<T>(__expf(gC - g[t]) * to_f32(KT[vk_off<T>(n, t)]));
       }
       frag_put<T, C>(Kt, n, gq, y);
     }
   }
   __syncthreads();
-  // X = A21 T11 (32 x 32 x 32), then T21 = -T22 X; four entries per thread.
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int e = tid + q * NT, i = e >> 5, jj = e & 31;
-    float x = 0.f;
-#pragma unroll 8
-    for (int sx = jj; sx < 32; ++sx) x += Am[(32 + i) * C + sx] * Tf[sx * TP + jj];
-    Xb[i * 33 + jj] = x;
+  if (wave < 2) {  // level 1, block p = wave; scratch Y_p at rows 16 p.., columns 32..47
+    const int p = wave, o = 32 * p;
+    put16<MP>(M, 16 * p, 32, mm16<MP>(M, o + 16, o, o, o, 0, 4), 1.f);
+    put16<MP>(M, o + 16, o, mm16<MP>(M, o + 16, o + 16, 16 * p, 32, 0, 4), -1.f);
   }
   __syncthreads();
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int e = tid + q * NT, i = e >> 5, jj = e & 31;
-    float x = 0.f;
-#pragma unroll 8
-    for (int sx = 0; sx <= i; ++sx) x -= Tf[(32 + i) * TP + 32 + sx] * Xb[sx * 33 + jj];
-    Tf[(32 + i) * TP + jj] = x;
+  {  // level 2, X = A21 T11: tile (a, bb) of the 32 x 32 result per wave, to rows 0..31,
+     // columns 32..63 (T11 is lower triangular: k from 16 bb)
+    const int a = wave >> 1, bb = wave & 1;
+    put16<MP>(M, 16 * a, 32 + 16 * bb, mm16<MP>(M, 32 + 16 * a, 0, 0, 16 * bb, 4 * bb, 8 - 4 * bb), 1.f);
   }
   __syncthreads();
-  // The products need T diag(beta) and T diag(beta gamma) in the call dtype.
-  for (int e = tid; e < C * C; e += NT) {
-    const int i = e >> 6, jj = e & 63;
-    const float t = Tf[i * TP + jj];
-    Tu[i * L::TWP + jj] = from_f32<T>(t * bet[jj]);
-    Tw[i * L::TWP + jj] = from_f32<T>(t * bet[jj] * __expf(g[jj]));
+  {  // T21 = -T22 X over A21's place (T22 is lower triangular: k up to 16 a + 15)
+    const int a = wave >> 1, bb = wave & 1;
+    put16<MP>(M, 32 + 16 * a, 16 * bb, mm16<MP>(M, 32 + 16 * a, 32, 0, 32 + 16 * bb, 0, 4 + 4 * a), -1.f);
   }
   __syncthreads();
 
-  // 5. Uv = (T diag(beta)) V and W = (T diag(beta gamma)) K, 32x32 tiles over the waves. Uv
-  //    comes out with a value column per lane and W, computed as K^T (T diag(beta gamma))^T, with
-  //    a token per lane, so both store rows of their fragment-order form (Uv^T and -W): items
+  // 5. Uv = (T diag(beta)) V and W = (T diag(beta gamma)) K: waves 0, 1 the Uv row tiles 0, 1 and
+  //    waves 2, 3 the W row tiles, each over every column tile. The scaled rows of T are formed
+  //    in the call dtype as they are read (row tile 0 of T is zero beyond column 31). Uv comes
+  //    out with a value column per lane and W, computed as K^T (T diag(beta gamma))^T, with a
+  //    token per lane, so both store rows of their fragment-order form (Uv^T and -W): items
   //    8 q .. 8 q + 7 of a tile are logical positions 16 q + 8 h .. + 7 of the lane's row.
-  constexpr int NU = (C / 32) * (DV / 32), NW = (C / 32) * (DK / 32);
-  T* rec = ws.rec<T>(seq * NC + c);
-  for (int q = wave; q < NU + NW; q += NT / 64) {
-    const bool isu = q < NU;
-    const int qq = isu ? q : q - NU;
-    const int nd = isu ? DV / 32 : DK / 32;
-    const int ti = qq / nd, ni = qq % nd;
-    f32x16 acc = {};
+  {
+    const bool isu = wave < 2;
+    const int ti = wave & 1, nks = ti == 0 ? 2 : 4;
+    const float* sc = isu ? bet : bgm;
+    F tf[4];
 #pragma unroll
-    for (int ks = 0; ks < C / 16; ++ks) {
-      const int ko = ks * 16 + h * 8;
-      if (isu)
-        mfma_k16(acc, frag_load<T>(Tu + (ti * 32 + rr) * L::TWP + ko), frag_load<T>(VT + (ni * 32 + rr) * CP + ko));
-      else
-        mfma_k16(acc, frag_load<T>(KT + (ni * 32 + rr) * CP + ko), frag_load<T>(Tw + (ti * 32 + rr) * L::TWP + ko));
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < nks) {
+        const float* row = M + (ti * 32 + rr) * MP + ks * 16 + h * 8;
+        const f32x4 lo = *(const f32x4*)row, hi = *(const f32x4*)(row + 4);
+        const f32x4 slo = *(const f32x4*)(sc + ks * 16 + h * 8), shi = *(const f32x4*)(sc + ks * 16 + h * 8 + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          tf[ks][e] = from_f32<T>(lo[e] * slo[e]);
+          tf[ks][e + 4] = from_f32<T>(hi[e] * shi[e]);
+        }
+      }
     }
-    if (isu) {
+    T* rec = ws.rec<T>(seq * NC + c);
+    const int nd = isu ? DV / 32 : DK / 32;
+    for (int ni = 0; ni < nd; ++ni) {
+      f32x16 acc = {};
 #pragma unroll
-      for (int qh = 0; qh < 2; ++qh)
-        frag_put<T, C>(rec + GdrRec<T, DK, DV>::UV, ni * 32 + rr, ti * 4 + 2 * qh + h, acc_frag<T>(acc, qh));
-    } else {
+      for (int ks = 0; ks < 4; ++ks) {
+        if (ks < nks) {
+          if (isu)
+            mfma_k16(acc, tf[ks], vk_frag<T>(VT, ni * 32 + rr, ks * 16 + h * 8));
+          else
+            mfma_k16(acc, vk_frag<T>(KT, ni * 32 + rr, ks * 16 + h * 8), tf[ks]);
+        }
+      }
+      if (isu) {
 #pragma unroll
-      for (int qh = 0; qh < 2; ++qh)
-        frag_put<T, DK>(rec, ti * 32 + rr, ni * 4 + 2 * qh + h, acc_frag<T>(-acc, qh));
+        for (int qh = 0; qh < 2; ++qh)
+          frag_put<T, C>(rec + GdrRec<T, DK, DV>::UV, ni * 32 + rr, ti * 4 + 2 * qh + h, acc_frag<T>(acc, qh));
+      } else {
+#pragma unroll
+        for (int qh = 0; qh < 2; ++qh)
+          frag_put<T, DK>(rec, ti * 32 + rr, ni * 4 + 2 * qh + h, acc_frag<T>(-acc, qh));
+      }
     }
   }
   if (tid == 0) ws.gc[seq * NC + c] = __expf(gC);
