@@ -19,16 +19,17 @@ ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function"]
-DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-# Per-source device options. The delta-rule chain keeps its state in MFMA accumulators and
-# works on them with VALU every step; the VGPR form of the MFMA instructions keeps them out of
-# the AGPR file, which would otherwise cost a copy each way per element and step.
-EXTRA = {"delta_rule.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# The VGPR form of the MFMA instructions keeps accumulators out of the AGPR file. Kernels that
+# work on their accumulators with VALU inside their main loops (online softmax, the delta-rule
+# chain) otherwise pay a copy each way per element and step; the dense GEMM main loops compile
+# to the same code either way.
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def _compile(src: str) -> str:
     out = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC] + COMMON + DEVICE + EXTRA.get(src, []) + ["-I", CSRC, "-c", os.path.join(CSRC, src), "-o", out]
+    cmd = [HIPCC] + COMMON + DEVICE + ["-I", CSRC, "-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)

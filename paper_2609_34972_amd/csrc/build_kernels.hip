@@ -279,7 +279,6 @@ __global__ __launch_bounds__(DownP::NT) void k_down_act_p(const bf16* __restrict
 
 // Up-projection epilogue staging: the fp32 tile, rows padded by 4 floats so the transposed
 // accumulator writes (32 rows at one column per instruction) hit distinct banks.
-constexpr int kUpPitch = UpP::BN + 4;
 template <class C>
 constexpr int up_lds_bytes() {
   return C::BM * (C::BN + 4) * 4 > C::LDS_BYTES ? C::BM * (C::BN + 4) * 4 : C::LDS_BYTES;

@@ -37,7 +37,6 @@ namespace dv {
 
 namespace gdr {
 constexpr int C = 64;     // tokens per chunk
-constexpr int PAD = 8;    // elements of padding per LDS row (bank spread)
 constexpr int NT = 256;   // threads per block (4 waves)
 }  // namespace gdr
 
