@@ -394,6 +394,14 @@ __global__ __launch_bounds__(gdr::NT) void k_gdr_prep(const T* __restrict__ k,
   if (tid == 0) ws.gc[seq * NC + c] = __expf(gC);
 }
 
+// Offset of Phi[i][j] in a segment's transition matrix: fp32 rows of DK, 16-byte chunks XOR-
+// swizzled by the row, so that k_gdr_merge can copy the matrix into LDS as it is and read A
+// fragments (a row, two runs of four columns) without bank conflicts.
+template <int DK>
+__device__ __forceinline__ int phi_off(int i, int j) {
+  return i * DK + (((j >> 2) ^ (i & 15)) << 2) + (j & 3);
+}
+
 // LDS of k_gdr_chain: the chunk records in NS buffers (bf16: three, so that two records are in
 // flight while one is used; fp32: one). Per wave, a record copy is INS_PSI (with Uv) or INS_PHI
 // (without) 1 KiB instructions.
@@ -568,77 +576,100 @@ __global__ __launch_bounds__(gdr::NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
     stage = L::NS == 3 ? (stage == 2 ? 0 : stage + 1) : 0;
   }
   if (!active) return;
-  float* out;
-  int ld;
-  if (P == 1) {
-    out = S + seq * DK * DV;
-    ld = DV;
-  } else if (phi) {
-    out = ws.phi + (seq * P + seg) * DK * DK;
-    ld = DK;
-  } else {
-    out = ws.psi + (seq * P + seg) * DK * DV;
-    ld = DV;
+  if (phi) {
+    float* out = ws.phi + (seq * P + seg) * DK * DK;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) out[phi_off<DK>(kt * 32 + acc_row(lane, i), n0 + rr)] = st[kt][i];
+    return;
   }
+  float* out = P == 1 ? S + seq * DK * DV : ws.psi + (seq * P + seg) * DK * DV;
 #pragma unroll
   for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) out[(int64_t)(kt * 32 + acc_row(lane, i)) * ld + n0 + rr] = st[kt][i];
+    for (int i = 0; i < 16; ++i) out[(int64_t)(kt * 32 + acc_row(lane, i)) * DV + n0 + rr] = st[kt][i];
 }
 
 // S <- Phi_g S + Psi_g for g = 1 .. P-1, from S = Psi_0; grid (column blocks, Hv, B), 32 state
-// columns per wave. Phi_g is read as the A operand in the k order of the state's accumulators
-// (two runs of four fp32 per lane half) and rounded to the call dtype, as the chunk steps round
-// their operands.
+// columns per wave. The block copies each Phi_g into LDS once (two buffers, the next one in
+// flight) and every wave reads it as the A operand in the k order of the state's accumulators,
+// rounded to the call dtype as the chunk steps round their operands. Psi_g is loaded one step
+// ahead, before the next copy is issued, so that waiting for it never waits for the copy.
+template <typename T, int DK>
+struct MergeLds {
+  static constexpr int PHI_BYTES = DK * DK * 4;
+  static constexpr size_t bytes = 2 * (size_t)PHI_BYTES;
+  static constexpr int INS = PHI_BYTES / 1024 / (gdr::NT / 64);
+  static_assert(PHI_BYTES % (1024 * (gdr::NT / 64)) == 0, "every wave copies the same number of KiB");
+};
+
 template <typename T, int DK, int DV>
 __global__ __launch_bounds__(gdr::NT) void k_gdr_merge(float* __restrict__ S, int Hv, GdrWs ws) {
   typedef typename Frag8<T>::type F;
+  typedef MergeLds<T, DK> L;
   constexpr int NKT = DK / 32;
+  extern __shared__ __align__(16) unsigned char smem[];
   const int P = ws.P;
   const int hv = blockIdx.y, b = blockIdx.z;
   const int64_t seq = (int64_t)b * Hv + hv;
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int h = lane >> 5, rr = lane & 31;
   const int n0 = blockIdx.x * 128 + wave * 32;
-  if (n0 >= DV) return;
-  f32x16 st[NKT];
-  const float* Ps = ws.psi + seq * P * DK * DV + n0 + rr;
-#pragma unroll
-  for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) st[kt][i] = Ps[(int64_t)(kt * 32 + acc_row(lane, i)) * DV];
-  for (int g = 1; g < P; ++g) {
-    F sb[NKT][2];
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
-      sb[kt][0] = acc_frag<T>(st[kt], 0);
-      sb[kt][1] = acc_frag<T>(st[kt], 1);
-    }
-    const float* Pg = ws.psi + (seq * P + g) * DK * DV + n0 + rr;
+  const bool active = n0 < DV;  // inactive waves still copy and meet the barriers
+  const float* psi = ws.psi + seq * P * DK * DV + n0 + rr;
+  f32x16 st[NKT], ps[NKT];
+  auto load_psi = [&](int g, f32x16 (&x)[NKT]) {
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) st[kt][i] = Pg[(int64_t)(kt * 32 + acc_row(lane, i)) * DV];
-    const float* Phi = ws.phi + (seq * P + g) * DK * DK;
+      for (int i = 0; i < 16; ++i) x[kt][i] = psi[(int64_t)g * DK * DV + (int64_t)(kt * 32 + acc_row(lane, i)) * DV];
+  };
+  if (active) {
+    load_psi(0, st);
+    load_psi(1, ps);
+  }
+  gdr_copy_record(ws.phi + (seq * P + 1) * DK * DK, L::PHI_BYTES, smem, wave, L::PHI_BYTES / 1024);
+  for (int g = 1; g < P; ++g) {
+    const float* Phi = (const float*)(smem + (size_t)((g - 1) & 1) * L::PHI_BYTES);
+    // Phi_g and Psi_g have landed for this wave; the barrier makes that true of every wave and
+    // ends every wave's reads of the other buffer.
+    pipe_sync<waitcnt_imm(0, 0)>();
+    if (g + 1 < P)
+      gdr_copy_record(ws.phi + (seq * P + g + 1) * DK * DK, L::PHI_BYTES, smem + (size_t)(g & 1) * L::PHI_BYTES,
+                      wave, L::PHI_BYTES / 1024);
+    if (active) {
+      F sb[NKT][2];
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
-      const float* row = Phi + (int64_t)(kt * 32 + rr) * DK + 4 * h;
+      for (int kt = 0; kt < NKT; ++kt) {
+        sb[kt][0] = acc_frag<T>(st[kt], 0);
+        sb[kt][1] = acc_frag<T>(st[kt], 1);
+      }
 #pragma unroll
-      for (int k2 = 0; k2 < NKT; ++k2)
+      for (int kt = 0; kt < NKT; ++kt) st[kt] = ps[kt];
+      if (g + 1 < P) load_psi(g + 1, ps);
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const f32x4 lo = *(const f32x4*)(row + k2 * 32 + 16 * q);
-          const f32x4 hi = *(const f32x4*)(row + k2 * 32 + 16 * q + 8);
-          F a;
+      for (int kt = 0; kt < NKT; ++kt) {
+        const int i = kt * 32 + rr;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            a[e] = from_f32<T>(lo[e]);
-            a[e + 4] = from_f32<T>(hi[e]);
+        for (int k2 = 0; k2 < NKT; ++k2)
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const int j = k2 * 32 + 16 * q + 4 * h;
+            const f32x4 lo = *(const f32x4*)(Phi + phi_off<DK>(i, j));
+            const f32x4 hi = *(const f32x4*)(Phi + phi_off<DK>(i, j + 8));
+            F a;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              a[e] = from_f32<T>(lo[e]);
+              a[e + 4] = from_f32<T>(hi[e]);
+            }
+            mfma_k16(st[kt], a, sb[k2][q]);
           }
-          mfma_k16(st[kt], a, sb[k2][q]);
-        }
+      }
     }
   }
+  if (!active) return;
   float* Sg = S + seq * DK * DV + n0 + rr;
 #pragma unroll
   for (int kt = 0; kt < NKT; ++kt)
@@ -661,6 +692,7 @@ static hipError_t gdr_launch(const void* k, const void* v, const float* alpha, c
   static bool once = [] {
     allow_lds_bytes(k_gdr_prep<T, DK, DV>, LP::bytes);
     allow_lds_bytes(k_gdr_chain<T, DK, DV>, LC::bytes);
+    allow_lds_bytes(k_gdr_merge<T, DK, DV>, MergeLds<T, DK>::bytes);
     return true;
   }();
   (void)once;
@@ -677,7 +709,7 @@ static hipError_t gdr_launch(const void* k, const void* v, const float* alpha, c
   if (ws.P > 1) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    k_gdr_merge<T, DK, DV><<<dim3(gdr_xblocks(DV), Hv, B), gdr::NT, 0, s>>>(S, Hv, ws);
+    k_gdr_merge<T, DK, DV><<<dim3(gdr_xblocks(DV), Hv, B), gdr::NT, MergeLds<T, DK>::bytes, s>>>(S, Hv, ws);
   }
   record(ev.gdr_scan[1], s);
   return hipGetLastError();
