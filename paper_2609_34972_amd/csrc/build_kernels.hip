@@ -240,12 +240,11 @@ __device__ __forceinline__ void load4_bf16(const bf16* p, float (&x)[4]) {
   for (int e = 0; e < 4; ++e) x[e] = (float)v[e];
 }
 
-template <int ACT>
-__global__ __launch_bounds__(DownP::NT) void k_down_act_p(const bf16* __restrict__ E,
-                                                          const bf16* __restrict__ Dw,
-                                                          bf16* __restrict__ Z, int T, int d,
-                                                          int L, int r) {
-  typedef DownP C;
+template <class C, int ACT>
+__global__ __launch_bounds__(C::NT) void k_down_act_p(const bf16* __restrict__ E,
+                                                      const bf16* __restrict__ Dw,
+                                                      bf16* __restrict__ Z, int T, int d, int L,
+                                                      int r) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int N = L * r;
   const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
@@ -680,15 +679,34 @@ static hipError_t down_launch(const void* E, const void* Dw, void* Z, int T_, in
 hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, int d, int L,
                            int r, int act, int dtype, hipStream_t s, const LaunchEvents& ev) {
   if (dtype == 1) {
-    typedef DownP C;
-    dim3 grid(cdiv((int64_t)L * r, C::BN), cdiv(T_, C::BM));
+    // 256 x 256 tiles (one block per CU) once there are at least four rounds of them, so the
+    // last round's tail stays small; 128 x 128 tiles (two blocks per CU) below that.
+    static bool once = [] {
+      allow_lds(k_down_act_p<KvP, 0>, KvP::LDS_BYTES);
+      allow_lds(k_down_act_p<KvP, 1>, KvP::LDS_BYTES);
+      return true;
+    }();
+    (void)once;
+    const int64_t N = (int64_t)L * r;
+    const bool big = cdiv(N, KvP::BN) * cdiv(T_, KvP::BM) >= 4 * 256;
     record(ev.down[0], s);
-    if (act == 0)
-      k_down_act_p<0><<<grid, dim3(C::NT), C::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
-                                                              (bf16*)Z, (int)T_, d, L, r);
-    else
-      k_down_act_p<1><<<grid, dim3(C::NT), C::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
-                                                              (bf16*)Z, (int)T_, d, L, r);
+    if (big) {
+      dim3 grid(cdiv(N, KvP::BN), cdiv(T_, KvP::BM));
+      if (act == 0)
+        k_down_act_p<KvP, 0><<<grid, dim3(KvP::NT), KvP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
+                                                                         (bf16*)Z, (int)T_, d, L, r);
+      else
+        k_down_act_p<KvP, 1><<<grid, dim3(KvP::NT), KvP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
+                                                                         (bf16*)Z, (int)T_, d, L, r);
+    } else {
+      dim3 grid(cdiv(N, DownP::BN), cdiv(T_, DownP::BM));
+      if (act == 0)
+        k_down_act_p<DownP, 0><<<grid, dim3(DownP::NT), DownP::LDS_BYTES, s>>>(
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
+      else
+        k_down_act_p<DownP, 1><<<grid, dim3(DownP::NT), DownP::LDS_BYTES, s>>>(
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
+    }
     record(ev.down[1], s);
     return hipGetLastError();
   }

@@ -17,7 +17,9 @@ from tests.gpu_helpers import assert_close, cuda, f64, say
 
 pytestmark = pytest.mark.gpu
 
-BUILD_FULL = [configs.LLAVA7B, configs.QWEN25VL_VIDEO, configs.LLAVA_NEXT]
+BUILD_FULL = [configs.LLAVA7B, configs.QWEN25VL_VIDEO, configs.LLAVA_NEXT,
+              # 8241 tokens: the down projection's 256 x 256 tiles with a ragged last row tile
+              configs.LLAVA_NEXT.with_(name="next_ragged_tokens", B=3, Nv=2747)]
 ATTN_FULL = [configs.LLAVA7B, configs.QWEN25VL_VIDEO, configs.LLAVA_NEXT, configs.DECODE]
 
 
@@ -40,8 +42,8 @@ def test_full_build_sampled(w):
     torch.cuda.synchronize()
     del ws, wg
     rng = np.random.default_rng(1234)
-    # Z: 256 sampled tokens, every layer.
-    rows = np.sort(rng.choice(w.T, 256, replace=False))
+    # Z: 256 sampled tokens and the last 8, every layer.
+    rows = np.union1d(rng.choice(w.T, 256, replace=False), np.arange(w.T - 8, w.T))
     E64 = f64(E[torch.from_numpy(rows)])
     Zr = oracle.down(E64, f64(wts["Dw"]), w.act)
     Zg = f64(Z[:, torch.from_numpy(rows)])
@@ -49,7 +51,7 @@ def test_full_build_sampled(w):
         assert_close(Zg[l], Zr[l], w.dtype, f"Z layer {l}")
     # Kv / Vv: 64 sampled tokens, layers 0, L-1 and two random ones.
     layers = sorted({0, w.L - 1, *rng.choice(np.arange(1, w.L - 1), 2, replace=False).tolist()})
-    rows = np.sort(rng.choice(w.T, 64, replace=False))
+    rows = np.union1d(rng.choice(w.T, 64, replace=False), np.arange(w.T - 4, w.T))
     E64 = f64(E[torch.from_numpy(rows)])
     li = torch.tensor(layers)
     say(f"[full build {w.name}] oracle on {len(rows)} rows x layers {layers}")
