@@ -24,6 +24,8 @@ CASES = [
     # map, then the segments in order)
     SMALL.with_(name="dr_f32_segmented", B=1, Hk=1, Hv=2, N=4000, dk=128, dv=128),
     configs.GDN_IMAGE.with_(name="dr_bf16_segmented", B=2, Hk=2, Hv=4, N=4096),
+    SMALL.with_(name="dr_f32_dk64_segmented", B=1, Hk=1, Hv=2, N=4096),
+    configs.GDN_IMAGE.with_(name="dr_bf16_dk64_dv128_segmented", B=1, Hk=1, Hv=2, N=4100, dk=64, dv=128),
 ]
 
 
