@@ -218,7 +218,7 @@ def run_prefill(args, w):
     na = dvl.text_visual_attention_workspace(w.B, w.Hq, w.Hkv, w.hd, w.Nv, w.Nq, w.Nkt)
     ws_at = torch.empty(max(na, 16), dtype=torch.uint8, device=dev)
 
-    def step(ev=None):
+    def step(ev=None, attn_ev=None):
         if ev is not None:
             dvl.time_kernel(dvl.KERNEL_DOWN, *ev["down"])
             dvl.time_kernel(dvl.KERNEL_UP, *ev["up"])
@@ -226,20 +226,29 @@ def run_prefill(args, w):
         dvl.build_visual_memory(Eg, wg["Dw"], Z, act=w.act)
         dvl.project_visual_kv(Eg, Z, wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv, Vv, eps=w.eps,
                               ws=ws_kv)
+        if ev is not None:
+            for k in (dvl.KERNEL_DOWN, dvl.KERNEL_UP, dvl.KERNEL_KV):
+                dvl.time_kernel(k)
         for l in range(w.L):
-            if ev is not None:
-                dvl.time_kernel(dvl.KERNEL_ATTENTION, *ev["attn"][l])
+            if attn_ev is not None:
+                dvl.time_kernel(dvl.KERNEL_ATTENTION, *attn_ev[l])
             dvl.text_visual_attention(tg["Q"][l], Kv[l], Vv[l], tg["Kt"][l], tg["Vt"][l], O[l],
                                       q_pos0=w.q_pos0, ws=ws_at)
+        if attn_ev is not None:
+            dvl.time_kernel(dvl.KERNEL_ATTENTION)
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
+    # The timed steps bracket the three build launches with HIP events (the K/V projection is the
+    # roofline kernel). The 32 short attention launches are timed per kernel in separate steps
+    # after the timed region: events between them would add gaps to the measured step.
     hev = HipEvents()
-    evs = [{"down": hev.pair(), "up": hev.pair(), "kv": hev.pair(),
-            "attn": [hev.pair() for _ in range(w.L)]} for _ in range(args.steps)]
+    evs = [{"down": hev.pair(), "up": hev.pair(), "kv": hev.pair()} for _ in range(args.steps)]
+    n_attn_steps = 3
+    attn_evs = [[hev.pair() for _ in range(w.L)] for _ in range(n_attn_steps)]
     mk = lambda: torch.cuda.Event(enable_timing=True)
     t_begin, t_end = mk(), mk()
     marks = [mk() for _ in range(args.steps + 1)]
@@ -253,13 +262,14 @@ def run_prefill(args, w):
     t_end.record()
     torch.cuda.synchronize()
     step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
-    for k in (dvl.KERNEL_DOWN, dvl.KERNEL_UP, dvl.KERNEL_KV, dvl.KERNEL_ATTENTION):
-        dvl.time_kernel(k)
+    for s in range(n_attn_steps):
+        step(attn_ev=attn_evs[s])
+    torch.cuda.synchronize()
     ms_total = t_begin.elapsed_time(t_end)
     ms_step = ms_total / args.steps
     avg = lambda key: sum(hev.ms(e[key]) for e in evs) / args.steps
     ms_down, ms_up, ms_kv = avg("down"), avg("up"), avg("kv")
-    ms_attn_launch = sum(hev.ms(a) for e in evs for a in e["attn"]) / (args.steps * w.L)
+    ms_attn_launch = sum(hev.ms(a) for e in attn_evs for a in e) / (n_attn_steps * w.L)
     hev.close()
 
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -452,20 +462,25 @@ def run_delta(args, w, steps=None, warmup=None):
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    hev = HipEvents()
-    evs = [[(hev.pair(), hev.pair()) for _ in range(w.layers)] for _ in range(steps)]
+    # Steps timed without per-kernel events; the kernels are timed in extra steps afterwards.
     mk = lambda: torch.cuda.Event(enable_timing=True)
     marks = [mk() for _ in range(steps + 1)]
     for s_ in range(steps):
         marks[s_].record()
-        step(evs[s_])
+        step()
     marks[-1].record()
+    torch.cuda.synchronize()
+    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(steps)]
+    hev = HipEvents()
+    n_ev = min(steps, 3)
+    evs = [[(hev.pair(), hev.pair()) for _ in range(w.layers)] for _ in range(n_ev)]
+    for s_ in range(n_ev):
+        step(evs[s_])
     torch.cuda.synchronize()
     dvl.time_kernel(dvl.KERNEL_DELTA_PREP)
     dvl.time_kernel(dvl.KERNEL_DELTA_SCAN)
-    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(steps)]
-    prep = sum(hev.ms(e[0]) for st in evs for e in st) / (steps * w.layers)
-    scan = sum(hev.ms(e[1]) for st in evs for e in st) / (steps * w.layers)
+    prep = sum(hev.ms(e[0]) for st in evs for e in st) / (n_ev * w.layers)
+    scan = sum(hev.ms(e[1]) for st in evs for e in st) / (n_ev * w.layers)
     hev.close()
     ms = percentiles(step_ms)
     per_layer = ms["median"] / w.layers
@@ -517,18 +532,23 @@ def run_decode(args, w, layers_timed=None):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    hev = HipEvents()
-    evs = [[hev.pair() for _ in range(L)] for _ in range(args.steps)]
+    # Steps timed without per-kernel events; the kernels are timed in extra steps afterwards.
     mk = lambda: torch.cuda.Event(enable_timing=True)
     t0, t1 = mk(), mk()
     t0.record()
     for s in range(args.steps):
-        step(evs[s])
+        step()
     t1.record()
     torch.cuda.synchronize()
-    dvl.time_kernel(dvl.KERNEL_ATTENTION)
     ms_step = t0.elapsed_time(t1) / args.steps
-    ms_launch = sum(hev.ms(p) for e in evs for p in e) / (args.steps * L)
+    hev = HipEvents()
+    n_ev = min(args.steps, 3)
+    evs = [[hev.pair() for _ in range(L)] for _ in range(n_ev)]
+    for s in range(n_ev):
+        step(evs[s])
+    torch.cuda.synchronize()
+    dvl.time_kernel(dvl.KERNEL_ATTENTION)
+    ms_launch = sum(hev.ms(p) for e in evs for p in e) / (n_ev * L)
     hev.close()
     bytes_layer = configs.bytes_attention(w, layers=1)
     gbs = bytes_layer / (ms_launch * 1e-3) / 1e9
