@@ -253,26 +253,24 @@ __global__ __launch_bounds__(C::NT) void k_down_act_p(const bf16* __restrict__ E
                buffer_rsrc(E, 0), 1 << 30, ldb};
   BufOperand B{buffer_rsrc(Dw + (int64_t)n0 * d, (int64_t)(N - n0) * ldb),
                buffer_rsrc(Dw, 0), 1 << 30, ldb};
-  f32x16 acc[C::FM][C::FN];
+  f32x4 acc[C::FM][C::FN];
   pipe_mainloop<C>(A, B, d, (bf16*)smem, acc);
 
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
 #pragma unroll
   for (int a = 0; a < C::FM; ++a) {
-    const int row = m0 + wm * C::WM + a * 32 + (lane & 31);
+    const int row = m0 + wm * C::WM + a * 16 + pipe_row(lane);
     if (row >= T) continue;
 #pragma unroll
-    for (int b = 0; b < C::FN; ++b)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
-        if (n >= N) continue;
-        const int l = n / r, j = n - l * r;
-        const f32x16& v = acc[a][b];
-        store4_bf16(Z + ((int64_t)l * T + row) * r + j, v[4 * q], v[4 * q + 1], v[4 * q + 2],
-                    v[4 * q + 3], [](float x) { return ACT == 0 ? silu(x) : gelu(x); });
-      }
+    for (int b = 0; b < C::FN; ++b) {
+      const int n = n0 + wn * C::WN + b * 16 + pipe_col(lane);  // r % 16 == 0: one layer
+      if (n >= N) continue;
+      const int l = n / r, j = n - l * r;
+      const f32x4& v = acc[a][b];
+      store4_bf16(Z + ((int64_t)l * T + row) * r + j, v[0], v[1], v[2], v[3],
+                  [](float x) { return ACT == 0 ? silu(x) : gelu(x); });
+    }
   }
 }
 
@@ -315,7 +313,7 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
     const int row = m0 + r16 + i * (C::NT / 16);
     e_pre[i] = (row < T && col_ok) ? *(const u32x4*)(E + (int64_t)row * d + n0 + c8) : u32x4{};
   }
-  f32x16 acc[C::FM][C::FN];
+  f32x4 acc[C::FM][C::FN];
   pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
 
   // 1. Z_l U_l tile (fp32) into LDS. The main loop's last LDS read precedes its last barrier.
@@ -324,15 +322,10 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
   float* tile = (float*)smem;
 #pragma unroll
   for (int a = 0; a < C::FM; ++a) {
-    const int rl = wm * C::WM + a * 32 + (lane & 31);
+    const int rl = wm * C::WM + a * 16 + pipe_row(lane);
 #pragma unroll
     for (int b = 0; b < C::FN; ++b)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = wn * C::WN + b * 32 + pipe_col(lane, q);
-        const f32x16& v = acc[a][b];
-        *(f32x4*)(tile + rl * kUpPitch + c) = f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-      }
+      *(f32x4*)(tile + rl * kUpPitch + wn * C::WN + b * 16 + pipe_col(lane)) = acc[a][b];
   }
   __syncthreads();
   // 2. Rows of the tile: 16 lanes x 8 columns each cover the 128 columns, so E, gamma and the
@@ -442,11 +435,11 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
     sum += __shfl_xor(sum, 1, WAVE);
     if (half == 0) rs_lds[rr] = rsqrtf(sum / (float)d + eps);
   }
-  f32x16 acc[C::FM][C::FN];
+  f32x4 acc[C::FM][C::FN];
   pipe_mainloop<C>(A, B, d, (bf16*)smem, acc);  // its barriers also publish rs_lds
 
   // Epilogue through LDS: every wave writes its scaled 64 x 128 tile as bf16 rows (pitch padded
-  // by 16 B so the 32 rows written together hit distinct banks), then stores whole 16-byte
+  // by 16 B so the 16 rows written together hit distinct banks), then stores whole 16-byte
   // pieces: 16 lanes cover one 256-byte row, which lies inside one head of Kv or Vv.
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
@@ -455,27 +448,26 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
   __syncthreads();  // every wave is done with the pipeline stages
 #pragma unroll
   for (int a = 0; a < C::FM; ++a) {
-    const int rw = a * 32 + (lane & 31);  // row inside the wave tile
+    const int rw = a * 16 + pipe_row(lane);  // row inside the wave tile
     const float rs = rs_lds[wm * C::WM + rw];
 #pragma unroll
-    for (int b = 0; b < C::FN; ++b)
+    for (int b = 0; b < C::FN; ++b) {
+      const f32x4& v = acc[a][b];
+      const int cw = b * 16 + pipe_col(lane);  // first of this lane's 4 columns in the wave tile
+      float y[4] = {v[0] * rs, v[1] * rs, v[2] * rs, v[3] * rs};
+      if constexpr (EPI) {
+        const int n = n0 + wn * C::WN + cw;
+        const bf16* bias = n < kv ? epi.kb : epi.vb;
+        if (bias && n < N) {
+          float bb[4];
+          load4_bf16(bias + (int64_t)l * kv + (n < kv ? n : n - kv), bb);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const f32x16& v = acc[a][b];
-        float y[4] = {v[4 * q] * rs, v[4 * q + 1] * rs, v[4 * q + 2] * rs, v[4 * q + 3] * rs};
-        if constexpr (EPI) {
-          const int n = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
-          const bf16* bias = n < kv ? epi.kb : epi.vb;
-          if (bias && n < N) {
-            float bb[4];
-            load4_bf16(bias + (int64_t)l * kv + (n < kv ? n : n - kv), bb);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) y[u] += bb[u];
-          }
+          for (int u = 0; u < 4; ++u) y[u] += bb[u];
         }
-        bf16x4 o = {(bf16)y[0], (bf16)y[1], (bf16)y[2], (bf16)y[3]};
-        *(u32x2*)(ep + rw * EP + (b * 32 + pipe_col(lane, q)) * 2) = __builtin_bit_cast(u32x2, o);
       }
+      bf16x4 o = {(bf16)y[0], (bf16)y[1], (bf16)y[2], (bf16)y[3]};
+      *(u32x2*)(ep + rw * EP + cw * 2) = __builtin_bit_cast(u32x2, o);
+    }
   }
   __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));  // this wave's LDS writes landed
   const int64_t head_stride = (int64_t)Nv * hd;

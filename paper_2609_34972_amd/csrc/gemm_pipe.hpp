@@ -10,10 +10,15 @@
 //   16 rows read together by a fragment load land in 16 distinct bank groups. Lanes of a load
 //   instruction pick the global chunk that belongs at their LDS slot, so the swizzle costs
 //   nothing at load time.
+// * 16x16x32 MFMAs. With random bf16 operands the chip's clock (and so the MFMA rate) falls
+//   under load, and it falls less for this shape than for 32x32x16: a register-resident MFMA
+//   loop sustains about 1.9 PFLOP/s against 1.72 for 32x32x16 (both about 2.46 with constant
+//   operands). Every fragment still is one 16-byte LDS read per lane.
 // * The MFMA operands are swapped (acc = B-fragment x A-fragment), which leaves the transpose
-//   of the 32x32 tile in the accumulators: lane l holds row m = l % 32 of its fragment and four
-//   runs of four consecutive columns. Epilogues therefore see one output row per lane (per-row
-//   scales are per lane) and store 8-byte runs along the row.
+//   of the 16x16 tile in the accumulators: lane l holds row m = l % 16 of its fragment and one
+//   run of four consecutive columns starting at 4 * (l / 16). Epilogues therefore see one
+//   output row per lane and fragment (per-row scales are per lane) and store 8-byte runs along
+//   the row.
 #pragma once
 
 #include "dv_device.hpp"
@@ -53,13 +58,13 @@ struct PipeCfg {
   static constexpr int NWAVES = WGM * WGN, NT = WAVE * NWAVES;
   static constexpr int BK = 64;
   static constexpr int WM = BM / WGM, WN = BN / WGN;
-  static constexpr int FM = WM / 32, FN = WN / 32;
+  static constexpr int FM = WM / 16, FN = WN / 16;  // 16x16 accumulator fragments per wave
   static constexpr int A_INS = BM / 8 / NWAVES;  // 8-row (1 KiB) load instructions per wave
   static constexpr int B_INS = BN / 8 / NWAVES;
   static constexpr int INS = A_INS + B_INS;
   static constexpr int STAGE = (BM + BN) * BK;   // bf16 elements per stage
   static constexpr int LDS_BYTES = 2 * STAGE * 2;
-  static_assert(WM % 32 == 0 && WN % 32 == 0 && A_INS >= 1 && B_INS >= 1, "bad tile");
+  static_assert(WM % 16 == 0 && WN % 16 == 0 && A_INS >= 1 && B_INS >= 1, "bad tile");
 };
 
 // Lane byte offset inside an 8-row load block: LDS slot (row r = lane / 8, chunk pc = lane % 8)
@@ -98,26 +103,29 @@ __device__ __forceinline__ bf16x8 pipe_frag(const bf16* s, int row, int chunk) {
   return __builtin_bit_cast(bf16x8, *(const u32x4*)(s + row * 64 + pc * 8));
 }
 
+// Fragments of one 32-deep K step ks (0 or 1) of a 64-deep stage: lane l reads row l % 16 of
+// each 16-row fragment, K elements 8 * (l / 16) .. +7 of the step.
 template <class C>
 __device__ __forceinline__ void pipe_frags(const bf16* s, int ks, bf16x8 (&fa)[C::FM],
                                            bf16x8 (&fb)[C::FN]) {
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
-  const int chunk = ks * 2 + (lane >> 5);
+  const int chunk = ks * 4 + (lane >> 4);
   const bf16* sb = s + C::BM * C::BK;
 #pragma unroll
-  for (int a = 0; a < C::FM; ++a) fa[a] = pipe_frag(s, wm * C::WM + a * 32 + (lane & 31), chunk);
+  for (int a = 0; a < C::FM; ++a) fa[a] = pipe_frag(s, wm * C::WM + a * 16 + (lane & 15), chunk);
 #pragma unroll
-  for (int b = 0; b < C::FN; ++b) fb[b] = pipe_frag(sb, wn * C::WN + b * 32 + (lane & 31), chunk);
+  for (int b = 0; b < C::FN; ++b) fb[b] = pipe_frag(sb, wn * C::WN + b * 16 + (lane & 15), chunk);
 }
 
 template <class C>
-__device__ __forceinline__ void pipe_mfmas(f32x16 (&acc)[C::FM][C::FN], const bf16x8 (&fa)[C::FM],
+__device__ __forceinline__ void pipe_mfmas(f32x4 (&acc)[C::FM][C::FN], const bf16x8 (&fa)[C::FM],
                                            const bf16x8 (&fb)[C::FN]) {
 #pragma unroll
   for (int a = 0; a < C::FM; ++a)
 #pragma unroll
-    for (int b = 0; b < C::FN; ++b) mfma_k16(acc[a][b], fb[b], fa[a]);  // transposed tile
+    for (int b = 0; b < C::FN; ++b)  // transposed tile
+      acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[b], fa[a], acc[a][b], 0, 0, 0);
 }
 
 template <int IMM>
@@ -128,18 +136,19 @@ __device__ __forceinline__ void pipe_sync() {
   asm volatile("" ::: "memory");
 }
 
-// Column of accumulator item i of this lane inside its 32x32 fragment (the row is lane % 32):
-// items 4q..4q+3 are columns 8q + 4*(lane/32) + 0..3.
-__device__ __forceinline__ int pipe_col(int lane, int q) { return q * 8 + (lane >> 5) * 4; }
+// Accumulator item u (0..3) of fragment (a, b) of a wave holds row a*16 + pipe_row(lane) and
+// column b*16 + pipe_col(lane) + u of the wave tile.
+__device__ __forceinline__ int pipe_row(int lane) { return lane & 15; }
+__device__ __forceinline__ int pipe_col(int lane) { return (lane >> 4) * 4; }
 
 // A: block-tile rows start at A's first row; B likewise. K must be a multiple of 64.
 template <class C>
 __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOperand& B, int K,
-                                              bf16* lds, f32x16 (&acc)[C::FM][C::FN]) {
+                                              bf16* lds, f32x4 (&acc)[C::FM][C::FN]) {
 #pragma unroll
   for (int a = 0; a < C::FM; ++a)
 #pragma unroll
-    for (int b = 0; b < C::FN; ++b) acc[a][b] = f32x16{};
+    for (int b = 0; b < C::FN; ++b) acc[a][b] = f32x4{};
   const int va0 = pipe_lane_offset(A.ld_bytes, 0), va1 = pipe_lane_offset(A.ld_bytes, 1);
   const int vb0 = pipe_lane_offset(B.ld_bytes, 0), vb1 = pipe_lane_offset(B.ld_bytes, 1);
   const int nk = K / C::BK;
@@ -154,29 +163,25 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
   pipe_frags<C>(lds, 0, fa[0], fb[0]);
   for (int kt = 0; kt < nk; ++kt) {
     bf16* s = lds + (kt & 1) * C::STAGE;
+    // K step 0: the step-1 fragments are read between its MFMAs (issue order: a few MFMAs,
+    // then each fragment read followed by two MFMAs, so the reads overlap the matrix pipe).
+    pipe_frags<C>(s, 1, fa[1], fb[1]);
+    pipe_mfmas<C>(acc, fa[0], fb[0]);
+    constexpr int kLead = (C::FM * C::FN - 2 * (C::FM + C::FN)) / 2;
+    static_assert(kLead >= 0, "a K step needs two MFMAs per fragment read");
+    __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      if (ks < 3) {
-        pipe_frags<C>(s, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
-      } else {
-        // Every wave holds its last fragments of stage s and tile kt+1 has landed: refill s
-        // with tile kt+2 and fetch tile kt+1's first fragments before this tile's last MFMAs.
-        pipe_sync<waitcnt_imm(0, 0)>();
-        if (kt + 2 < nk) pipe_issue<C>(A, B, (kt + 2) * C::BK * 2, s, va0, va1, vb0, vb1);
-        if (kt + 1 < nk) pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
-      }
-      pipe_mfmas<C>(acc, fa[ks & 1], fb[ks & 1]);
-      if (ks < 3) {
-        // Issue order: two MFMAs, then each fragment read of the next K step followed by one
-        // MFMA, so the LDS reads overlap the matrix pipe instead of bunching up.
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-#pragma unroll
-        for (int i = 0; i < C::FM + C::FN; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        }
-      }
+    for (int i = 0; i < C::FM + C::FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kLead - 2 * (C::FM + C::FN), 0);
+    // K step 1: every wave holds its last fragments of stage s and tile kt+1 has landed:
+    // refill s with tile kt+2 and fetch tile kt+1's first fragments before this step's MFMAs.
+    pipe_sync<waitcnt_imm(0, 0)>();
+    if (kt + 2 < nk) pipe_issue<C>(A, B, (kt + 2) * C::BK * 2, s, va0, va1, vb0, vb1);
+    if (kt + 1 < nk) pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
+    pipe_mfmas<C>(acc, fa[1], fb[1]);
   }
 }
 

@@ -166,24 +166,21 @@ __global__ __launch_bounds__(RecP::NT) void k_down_partial_p(const bf16* __restr
                buffer_rsrc(X, 0), 1 << 30, ldb};
   BufOperand B{buffer_rsrc(Dl + (int64_t)n0 * d + k0, (int64_t)(r - n0) * ldb - (int64_t)k0 * 2),
                buffer_rsrc(Dl, 0), 1 << 30, ldb};
-  f32x16 acc[C::FM][C::FN];
+  f32x4 acc[C::FM][C::FN];
   pipe_mainloop<C>(A, B, klen, (bf16*)smem, acc);
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   float* ps = part + (int64_t)s * T * r;
 #pragma unroll
   for (int a = 0; a < C::FM; ++a) {
-    const int row = m0 + wm * C::WM + a * 32 + (lane & 31);
+    const int row = m0 + wm * C::WM + a * 16 + pipe_row(lane);
     if (row >= T) continue;
 #pragma unroll
-    for (int b = 0; b < C::FN; ++b)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int col = n0 + wn * C::WN + b * 32 + pipe_col(lane, q);
-        if (col >= r) continue;
-        const f32x16& v = acc[a][b];
-        *(f32x4*)(ps + (int64_t)row * r + col) = f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-      }
+    for (int b = 0; b < C::FN; ++b) {
+      const int col = n0 + wn * C::WN + b * 16 + pipe_col(lane);
+      if (col >= r) continue;
+      *(f32x4*)(ps + (int64_t)row * r + col) = acc[a][b];
+    }
   }
 }
 
@@ -231,7 +228,7 @@ __global__ __launch_bounds__(RecP::NT) void k_up_rec_p(const TIn* Min, float* Ms
                1 << 30, ldb};
   BufOperand B{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
                1 << 30, ldb};
-  f32x16 acc[C::FM][C::FN];
+  f32x4 acc[C::FM][C::FN];
   pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
 
   const int lane = threadIdx.x & 63, wave = wave_index();
@@ -239,15 +236,10 @@ __global__ __launch_bounds__(RecP::NT) void k_up_rec_p(const TIn* Min, float* Ms
   float* tile = (float*)smem;  // the main loop's last LDS read precedes its last barrier
 #pragma unroll
   for (int a = 0; a < C::FM; ++a) {
-    const int rl = wm * C::WM + a * 32 + (lane & 31);
+    const int rl = wm * C::WM + a * 16 + pipe_row(lane);
 #pragma unroll
     for (int b = 0; b < C::FN; ++b)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = wn * C::WN + b * 32 + pipe_col(lane, q);
-        const f32x16& v = acc[a][b];
-        *(f32x4*)(tile + rl * kRecPitch + c) = f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-      }
+      *(f32x4*)(tile + rl * kRecPitch + wn * C::WN + b * 16 + pipe_col(lane)) = acc[a][b];
   }
   __syncthreads();
   bf16x8 g8 = {};
