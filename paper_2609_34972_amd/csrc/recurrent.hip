@@ -270,7 +270,7 @@ __global__ __launch_bounds__(RecP::NT) void k_up_rec_p(const TIn* Min, float* Ms
       *(f32x4*)(Mst + at) = m0v;
       *(f32x4*)(Mst + at + 4) = m1v;
       if (Mop) *(u32x4*)(Mop + at) = __builtin_bit_cast(u32x4, o);
-      *(u32x4*)(Mg + at) = __builtin_bit_cast(u32x4, mg);
+      __builtin_nontemporal_store(__builtin_bit_cast(u32x4, mg), (u32x4*)(Mg + at));  // read only by the last launch
     }
     ss += shfl_xor(ss, 1);
     ss += shfl_xor(ss, 2);
