@@ -86,8 +86,8 @@ def load() -> ctypes.CDLL:
             return _lib
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(
-                f"{LIB_PATH} is missing: build it with `python -m paper_2609_34972_amd.build` "
-                "(or __graft_entry__.build()); there is no non-HIP implementation")
+                f"{LIB_PATH} is missing: build it with `python -m paper_2609_34972_amd.build`; "
+                "there is no non-HIP implementation")
         lib = ctypes.CDLL(LIB_PATH)
         vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
         lib.dv_build_visual_memory.argtypes = [vp, vp, vp, i64, i32, i32, i32, i32, i32, vp]
