@@ -335,6 +335,30 @@ __device__ __forceinline__ void online_softmax(float (&sv)[NI], float scale_log2
 // stating it is uniform keeps load bases and sizes in scalar registers.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Work of a prefill block: (batch * kv-head group bg, block of query rows rb, key split). The
+// dispatcher deals consecutive launch ids out to the 8 XCDs in turn, so ids congruent mod 8 run on
+// one XCD. All row blocks of one (bg, split) stream read the same K/V range: they get ids x,
+// x + 8, x + 16, ..., so that range comes from memory once into that XCD's L2. Streams left over
+// when their count is not a multiple of 8 are laid out contiguously.
+struct BlockWork {
+  int bg, rb, split;
+};
+__device__ __forceinline__ BlockWork block_work(int n_bg, int row_blocks, int splits) {
+  const int id = blockIdx.x + gridDim.x * blockIdx.y;
+  const int streams = n_bg * splits, full = (streams / 8) * 8 * row_blocks;
+  int s, rb;
+  if (id < full) {
+    const int slot = id / 8;
+    rb = slot % row_blocks;
+    s = (slot / row_blocks) * 8 + id % 8;
+  } else {
+    const int r = id - full;
+    rb = r % row_blocks;
+    s = (streams / 8) * 8 + r / row_blocks;
+  }
+  return BlockWork{uni(s / splits), uni(rb), uni(s % splits)};
+}
+
 // Wait until tile t+1 of the pipeline has landed when `ahead` later tiles may stay in flight
 // (never encoding more than the 63 loads vmcnt can count), then synchronise the block.
 template <int INS>
@@ -358,24 +382,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
   const int lane = threadIdx.x & 63, wave = wave_index(), g2 = lane >> 5;
   const int G = a.Hq / a.Hkv, R = a.Nq * G, n_bg = a.B * a.Hkv;
 
-  // Blocks id and id + 8 run on the same XCD; give them the same (batch, kv-head) so the
-  // row-blocks sharing one K/V stream share that XCD's L2.
-  int rb, bg;
-  {
-    const int id = blockIdx.x, full = (n_bg / 8) * 8 * row_blocks;
-    if (id < full) {
-      rb = (id / 8) % row_blocks;
-      bg = (id % 8) + 8 * (id / (8 * row_blocks));
-    } else {
-      const int r = id - full;
-      rb = r % row_blocks;
-      bg = (n_bg / 8) * 8 + r / row_blocks;
-    }
-  }
-  rb = uni(rb);
-  bg = uni(bg);
+  const BlockWork wk = block_work(n_bg, row_blocks, a.splits);
+  const int rb = wk.rb, bg = wk.bg, split = wk.split;
   const int b = uni(bg / a.Hkv), g = bg - b * a.Hkv;
-  const int split = blockIdx.y;
   const int row0 = rb * 32 * NW;
   const int my_row = row0 + wave * 32 + (lane & 31);
   const bool row_ok = my_row < R;
@@ -582,22 +591,9 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
 
   const int lane = threadIdx.x & 63, wave = wave_index(), g2 = lane >> 5;
   const int G = a.Hq / a.Hkv, R = a.Nq * G, n_bg = a.B * a.Hkv;
-  int rb, bg;  // blocks id and id + 8 share an XCD: give them the same (batch, kv-head)
-  {
-    const int id = blockIdx.x, full = (n_bg / 8) * 8 * row_blocks;
-    if (id < full) {
-      rb = (id / 8) % row_blocks;
-      bg = (id % 8) + 8 * (id / (8 * row_blocks));
-    } else {
-      const int r = id - full;
-      rb = r % row_blocks;
-      bg = (n_bg / 8) * 8 + r / row_blocks;
-    }
-  }
-  rb = uni(rb);
-  bg = uni(bg);
+  const BlockWork wk = block_work(n_bg, row_blocks, a.splits);
+  const int rb = wk.rb, bg = wk.bg, split = wk.split;
   const int b = uni(bg / a.Hkv), g = bg - b * a.Hkv;
-  const int split = blockIdx.y;
   const int row0 = rb * 32;
   const int my_row = row0 + (lane & 31);
   const bool row_ok = my_row < R;
