@@ -282,6 +282,9 @@ constexpr int up_lds_bytes() {
 }
 constexpr int kUpLdsBytes = up_lds_bytes<UpP>();
 
+// Layers per block of the up projection: the block's tile of E is read once for all of them.
+constexpr int kUpLayers = 4;
+
 template <class C>
 __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        const bf16* __restrict__ Z,
@@ -289,20 +292,14 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        const bf16* __restrict__ gamma,
                                                        bf16* __restrict__ Mg,
                                                        float* __restrict__ ssq, int T, int d,
-                                                       int r, int l0) {
+                                                       int r, int l0, int nl) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int kUpPitch = C::BN + 4;
-  const int lz = blockIdx.z, l = l0 + lz;
   const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
-  const bf16* Zl = Z + (int64_t)l * T * r;
-  const bf16* Ul = Uw + (int64_t)l * d * r;
+  const int lz_begin = blockIdx.z * kUpLayers, lz_end = min(nl, lz_begin + kUpLayers);
   const int ldb = r * 2;
-  BufOperand A{buffer_rsrc(Zl + (int64_t)m0 * r, (int64_t)(T - m0) * ldb), buffer_rsrc(Zl, 0),
-               1 << 30, ldb};
-  BufOperand B{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
-               1 << 30, ldb};
   // The epilogue's rows of E (16 lanes x 16 bytes per 128-column row, BM/16 rows per thread)
-  // are fetched before the main loop so they arrive while the MFMAs run.
+  // are fetched once, before the first main loop, and serve every layer of the block.
   constexpr int kRows = C::BM / (C::NT / 16);
   const int c8 = (threadIdx.x & 15) * 8;
   const int r16 = threadIdx.x >> 4;
@@ -313,54 +310,65 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
     const int row = m0 + r16 + i * (C::NT / 16);
     e_pre[i] = (row < T && col_ok) ? *(const u32x4*)(E + (int64_t)row * d + n0 + c8) : u32x4{};
   }
-  f32x4 acc[C::FM][C::FN];
-  pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
-
-  // 1. Z_l U_l tile (fp32) into LDS. The main loop's last LDS read precedes its last barrier.
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
-  float* tile = (float*)smem;
-#pragma unroll
-  for (int a = 0; a < C::FM; ++a) {
-    const int rl = wm * C::WM + a * 16 + pipe_row(lane);
-#pragma unroll
-    for (int b = 0; b < C::FN; ++b)
-      *(f32x4*)(tile + rl * kUpPitch + wn * C::WN + b * 16 + pipe_col(lane)) = acc[a][b];
-  }
-  __syncthreads();
-  // 2. Rows of the tile: 16 lanes x 8 columns each cover the 128 columns, so E, gamma and the
-  //    output move as whole 16-byte pieces of a row, and the row's sum of squares over this
-  //    column tile is a 16-lane shuffle.
-  const bf16* gl = gamma + (int64_t)l * d;
-  bf16* Ml = Mg + (int64_t)lz * T * d;
   const int np = (d + C::BN - 1) / C::BN;
-  bf16x8 g8 = {};
-  if (col_ok) g8 = __builtin_bit_cast(bf16x8, *(const u32x4*)(gl + n0 + c8));
+  float* tile = (float*)smem;
+  for (int lz = lz_begin; lz < lz_end; ++lz) {
+    const int l = l0 + lz;
+    const bf16* Zl = Z + (int64_t)l * T * r;
+    const bf16* Ul = Uw + (int64_t)l * d * r;
+    BufOperand A{buffer_rsrc(Zl + (int64_t)m0 * r, (int64_t)(T - m0) * ldb), buffer_rsrc(Zl, 0),
+                 1 << 30, ldb};
+    BufOperand B{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
+                 1 << 30, ldb};
+    bf16x8 g8 = {};
+    if (col_ok) g8 = __builtin_bit_cast(bf16x8, *(const u32x4*)(gamma + (int64_t)l * d + n0 + c8));
+    f32x4 acc[C::FM][C::FN];
+    // Its first wait also covers the previous layer's stores, which precede its loads.
+    pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
+
+    // 1. Z_l U_l tile (fp32) into LDS. The main loop's last LDS read precedes its last barrier.
 #pragma unroll
-  for (int i = 0; i < kRows; ++i) {
-    const int rr = r16 + i * (C::NT / 16);
-    const int row = m0 + rr;
-    float ss = 0.f;
-    if (row < T && col_ok) {
-      const bf16x8 e8 = __builtin_bit_cast(bf16x8, e_pre[i]);
-      const f32x4 p0 = *(const f32x4*)(tile + rr * kUpPitch + c8);
-      const f32x4 p1 = *(const f32x4*)(tile + rr * kUpPitch + c8 + 4);
-      bf16x8 o;
+    for (int a = 0; a < C::FM; ++a) {
+      const int rl = wm * C::WM + a * 16 + pipe_row(lane);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float m = (u < 4 ? p0[u] : p1[u - 4]) + (float)e8[u];
-        ss += m * m;
-        o[u] = (bf16)(m * (float)g8[u]);
-      }
-      // Streaming store: M * gamma of all layers (0.6 GB at LLaVA-7B shapes) is read only by the
-      // projection launch; through the caches the stores ran at about 1.8 TB/s.
-      __builtin_nontemporal_store(__builtin_bit_cast(u32x4, o), (u32x4*)(Ml + (int64_t)row * d + n0 + c8));
+      for (int b = 0; b < C::FN; ++b)
+        *(f32x4*)(tile + rl * kUpPitch + wn * C::WN + b * 16 + pipe_col(lane)) = acc[a][b];
     }
-    ss += shfl_xor(ss, 1);
-    ss += shfl_xor(ss, 2);
-    ss += shfl_xor(ss, 4);
-    ss += shfl_xor(ss, 8);
-    if ((threadIdx.x & 15) == 0 && row < T) ssq[((int64_t)lz * np + blockIdx.x) * T + row] = ss;
+    __syncthreads();
+    // 2. Rows of the tile: 16 lanes x 8 columns each cover the 128 columns, so E, gamma and the
+    //    output move as whole 16-byte pieces of a row, and the row's sum of squares over this
+    //    column tile is a 16-lane shuffle.
+    bf16* Ml = Mg + (int64_t)lz * T * d;
+#pragma unroll
+    for (int i = 0; i < kRows; ++i) {
+      const int rr = r16 + i * (C::NT / 16);
+      const int row = m0 + rr;
+      float ss = 0.f;
+      if (row < T && col_ok) {
+        const bf16x8 e8 = __builtin_bit_cast(bf16x8, e_pre[i]);
+        const f32x4 p0 = *(const f32x4*)(tile + rr * kUpPitch + c8);
+        const f32x4 p1 = *(const f32x4*)(tile + rr * kUpPitch + c8 + 4);
+        bf16x8 o;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float m = (u < 4 ? p0[u] : p1[u - 4]) + (float)e8[u];
+          ss += m * m;
+          o[u] = (bf16)(m * (float)g8[u]);
+        }
+        // Streaming store: M * gamma of all layers (0.6 GB at LLaVA-7B shapes) is read only by
+        // the projection launch; through the caches the stores ran at about 1.8 TB/s.
+        __builtin_nontemporal_store(__builtin_bit_cast(u32x4, o),
+                                    (u32x4*)(Ml + (int64_t)row * d + n0 + c8));
+      }
+      ss += shfl_xor(ss, 1);
+      ss += shfl_xor(ss, 2);
+      ss += shfl_xor(ss, 4);
+      ss += shfl_xor(ss, 8);
+      if ((threadIdx.x & 15) == 0 && row < T) ssq[((int64_t)lz * np + blockIdx.x) * T + row] = ss;
+    }
+    __syncthreads();  // the staging tile is read before the next layer's loads overwrite it
   }
 }
 
@@ -759,11 +767,11 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
   (void)once;
   const int T_ = B_ * Nv;
   const int np = cdiv(d, UpP::BN);
-  dim3 gu(np, cdiv(T_, UpP::BM), nl);
+  dim3 gu(np, cdiv(T_, UpP::BM), cdiv(nl, kUpLayers));
   if (first) record(ev.up[0], s);
   k_up_norm_p<UpP><<<gu, dim3(UpP::NT), kUpLdsBytes, s>>>(
       (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_, d, r,
-      l0);
+      l0, nl);
   if (last) record(ev.up[1], s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
