@@ -65,6 +65,9 @@ MID = [
     # GQA, hd = 64, a hidden size that is not a multiple of the 128-column tile
     configs.QWEN25VL_VIDEO.with_(name="mid_gqa_hd64", d=960, L=3, r=64, Hq=8, Hkv=2, hd=64, B=3,
                                  Nv=37, Nt=16),
+    # Few column tiles (2 kv x 4 heads x 128 = 4 tiles of 256) and many more rows than columns: the
+    # projection deals its row tiles out to the XCDs; 12 row tiles, 4 of them past the first 8
+    configs.QWEN25VL_VIDEO.with_(name="mid_rows_dealt", d=256, L=2, r=64, B=3, Nv=1000, Nt=16),
     # fp32 with several tiles in every dimension
     configs.TINY.with_(name="mid_f32", d=320, L=5, r=48, Hq=6, Hkv=3, hd=128, B=2, Nv=70,
                        act=configs.ACT_SILU),
