@@ -942,10 +942,14 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float* __restrict__ 
   if (t >= rows * CPR) return;
   const int64_t row = t / CPR;
   const int c = (int)(t - row * CPR) * 4;
+  // Unrolled so that several splits' loads are in flight at once: the partials were written by
+  // blocks on every XCD and come from beyond this XCD's L2.
   float mx = NEG_BIG;
+#pragma unroll 8
   for (int s = 0; s < splits; ++s) mx = fmaxf(mx, MLpart[((int64_t)s * rows + row) * 2]);
   float lt = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
   for (int s = 0; s < splits; ++s) {
     const float* ml = MLpart + ((int64_t)s * rows + row) * 2;
     const float sc = exp2f(ml[0] - mx);
