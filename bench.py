@@ -194,6 +194,30 @@ def cpu_baseline(w, E, wts, tx, vcache):
     }
 
 
+def mfma_probe(iters=2048, reps=3):
+    """Sustained bf16 MFMA rate of this GPU on register operands (no memory traffic), on random
+    and on constant operands: the clock, and so the rate, depends on how much the operands toggle.
+    Runs outside every timed region."""
+    import torch
+
+    import paper_2609_34972_amd as dvl
+    sink = torch.empty(dvl.PROBE_BLOCKS, dtype=torch.float32, device="cuda:0")
+    out = {"iters": iters}
+    for name, rnd in (("random_bf16_tflops", True), ("constant_tflops", False)):
+        dvl.probe_mfma(rnd, 256, sink)
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            dvl.probe_mfma(rnd, iters, sink)
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        ts.sort()
+        out[name] = dvl.PROBE_FLOP_PER_ITER * iters / (ts[len(ts) // 2] * 1e-3) / 1e12
+    return out
+
+
 def run_prefill(args, w):
     import torch
 
@@ -317,6 +341,11 @@ def run_prefill(args, w):
         },
     }
     out["step_ms_warm"] = percentiles(step_ms)
+    if w.dtype == "bf16":
+        log("[bench] MFMA-rate probe")
+        probe = mfma_probe()
+        probe["kernel_frac_of_random"] = kv_tflops / probe["random_bf16_tflops"]
+        out["roofline"]["mfma_probe"] = probe
     if not args.no_cold:
         log("[bench] cold steps (512 MiB rewritten between steps)")
         flush = torch.empty(128 << 20, dtype=torch.float32, device=dev)

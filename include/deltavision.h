@@ -256,6 +256,18 @@ typedef enum {
 } dv_kernel;
 dv_status dv_time_kernel(int32_t kernel, void* ev_begin, void* ev_end);
 
+/* Measurement probe, not part of the method: the sustained bf16 MFMA rate of this GPU. The
+ * chip's clock drops under MFMA load, and drops further the more the operand bits toggle, so the
+ * rate a GEMM can reach depends on its data. The probe enqueues 1024 blocks of 8 waves; each wave
+ * issues iters x 32 independent v_mfma_f32_16x16x32_bf16 (the instruction of the build GEMMs) on
+ * register operands, with no memory traffic, and block b writes one float to sink[b].
+ *   random  != 0: operands are random bf16 bit patterns (spread exponents, random mantissas);
+ *           0: constant operands.
+ *   iters   in [1, 1 << 20]; the call performs 1024 * 8 * iters * 32 * 16384 FLOP.
+ *   sink    device memory of at least 1024 floats, caller-owned, 16-byte aligned.
+ * Time it with events on `stream` around the call. */
+dv_status dv_probe_mfma(int32_t random, int32_t iters, float* sink, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* dv_status_string(int32_t status);
 /* Detail of the last error raised on the calling thread ("" if none). */

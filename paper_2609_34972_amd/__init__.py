@@ -9,9 +9,11 @@ Eq. 9). The arithmetic runs in hand-written HIP kernels behind the C ABI of
 """
 from ._lib import (ACT_GELU, ACT_SILU, KERNEL_ATTENTION, KERNEL_DELTA_PREP, KERNEL_DELTA_SCAN,
                    KERNEL_DOWN, KERNEL_KV, KERNEL_UP,
+                   PROBE_BLOCKS, PROBE_FLOP_PER_ITER,
                    DeltaVisionError, KVEpilogue, build_visual_memory, delta_rule_workspace,
                    delta_rule_write, kept_visual_kv,
-                   kept_visual_kv_workspace, load, project_visual_kv, project_visual_kv_ex_workspace,
+                   kept_visual_kv_workspace, load, probe_mfma, project_visual_kv,
+                   project_visual_kv_ex_workspace,
                    project_visual_kv_workspace, recurrent_visual_kv,
                    recurrent_visual_kv_workspace, text_visual_attention,
                    text_visual_attention_workspace, time_kernel)
@@ -24,5 +26,5 @@ __all__ = [
     "text_visual_attention",
     "text_visual_attention_workspace", "time_kernel", "KERNEL_DOWN", "KERNEL_UP", "KERNEL_KV",
     "KERNEL_ATTENTION", "KERNEL_DELTA_PREP", "KERNEL_DELTA_SCAN", "delta_rule_write",
-    "delta_rule_workspace",
+    "delta_rule_workspace", "probe_mfma", "PROBE_BLOCKS", "PROBE_FLOP_PER_ITER",
 ]

@@ -31,6 +31,7 @@ EXPORTS = (
     "dv_status_string",
     "dv_last_error",
     "dv_abi_version",
+    "dv_probe_mfma",
     "dv_time_kernel",
     "dv_recurrent_visual_kv_workspace",
     "dv_recurrent_visual_kv",
@@ -116,6 +117,8 @@ def load() -> ctypes.CDLL:
         lib.dv_abi_version.restype = i32
         lib.dv_time_kernel.argtypes = [i32, vp, vp]
         lib.dv_time_kernel.restype = i32
+        lib.dv_probe_mfma.argtypes = [i32, i32, vp, vp]
+        lib.dv_probe_mfma.restype = i32
         lib.dv_recurrent_visual_kv_workspace.argtypes = [i64, i32, i32, i32, i32]
         lib.dv_recurrent_visual_kv_workspace.restype = sz
         lib.dv_recurrent_visual_kv.argtypes = [vp] * 8 + [i32] * 8 + [f32, i32, vp, sz, vp]
@@ -166,6 +169,18 @@ def time_kernel(kernel: int, begin: Optional[int] = None, end: Optional[int] = N
     """Bracket every later launch of `kernel` on this thread with two hipEvent_t handles
     (raw integers, e.g. from hipEventCreate); time_kernel(kernel) switches the hook off."""
     _check(load().dv_time_kernel(kernel, begin, end))
+
+
+PROBE_BLOCKS = 1024
+PROBE_FLOP_PER_ITER = 1024 * 8 * 32 * 2 * 16 * 16 * 32  # blocks x waves x MFMAs x FLOP per MFMA
+
+
+def probe_mfma(random: bool, iters: int, sink: torch.Tensor, stream=None) -> None:
+    """Enqueue the MFMA-rate probe (iters x PROBE_FLOP_PER_ITER FLOP on register operands);
+    sink is a float32 CUDA tensor of at least PROBE_BLOCKS elements."""
+    if sink.dtype != torch.float32 or sink.numel() < PROBE_BLOCKS or not sink.is_cuda:
+        raise ValueError("sink must be a float32 CUDA tensor of at least 1024 elements")
+    _check(load().dv_probe_mfma(1 if random else 0, iters, _ptr(sink), _stream(sink.device, stream)))
 
 
 def build_visual_memory(E: torch.Tensor, Dw: torch.Tensor, Z: torch.Tensor, act: int = ACT_SILU,

@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdeltavision.so")
-SOURCES = ["api.cpp", "build_kernels.hip", "attention.hip", "recurrent.hip", "delta_rule.hip"]
+SOURCES = ["api.cpp", "build_kernels.hip", "attention.hip", "recurrent.hip", "delta_rule.hip",
+           "probe.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -13,6 +13,7 @@
 #include "attention.hpp"
 #include "build_kernels.hpp"
 #include "delta_rule.hpp"
+#include "probe.hpp"
 
 namespace {
 
@@ -109,6 +110,15 @@ dv_status dv_time_kernel(int32_t kernel, void* ev_begin, void* ev_end) {
   }
   slot[0] = (hipEvent_t)ev_begin;
   slot[1] = (hipEvent_t)ev_end;
+  return ok();
+}
+
+dv_status dv_probe_mfma(int32_t random, int32_t iters, float* sink, void* stream) {
+  DV_CHECK(need_ptr(sink, "sink"));
+  if (iters < 1 || iters > (1 << 20))
+    return fail(DV_ERR_SHAPE, "iters=%d must lie in [1, 2^20]", iters);
+  if (dv::launch_probe_mfma(random != 0, iters, sink, (hipStream_t)stream) != hipSuccess)
+    return fail(DV_ERR_HIP, "probe launch failed");
   return ok();
 }
 

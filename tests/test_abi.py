@@ -287,3 +287,12 @@ def test_delta_rule_workspace_scales_with_chunks(lib):
     assert one >= 32 * (64 * 128 * 3 * 2 + 4)
     assert lib.dv_delta_rule_workspace(1, 32, 65, 128, 128, BF16) > one  # a second chunk
     assert lib.dv_delta_rule_workspace(1, 32, 64, 96, 128, BF16) == 0
+
+
+@pytest.mark.parametrize("sink,iters,code", [
+    (None, 16, NULL), (FAKE + 4, 16, ALIGN), (FAKE, 0, SHAPE), (FAKE, -1, SHAPE),
+    (FAKE, (1 << 20) + 1, SHAPE),
+])
+def test_probe_mfma_rejects(lib, sink, iters, code):
+    assert lib.dv_probe_mfma(1, iters, sink, None) == code
+    assert lib.dv_last_error() != b""

@@ -215,3 +215,18 @@ def test_rejects_bad_shapes_without_writing():
     assert ei.value.name == "DV_ERR_SHAPE"
     torch.cuda.synchronize()
     assert bool(torch.all(O == 7.0))
+
+
+def test_mfma_probe():
+    """The measurement probe runs the MFMAs it is timed for: with constant operands (bf16 1.0)
+    every accumulator gains 32 per MFMA, so block sinks read 32 fragments x 4 lanes' items x
+    32 x iters."""
+    say("[mfma probe]")
+    sink = torch.full((dvl.PROBE_BLOCKS,), float("nan"), dtype=torch.float32, device="cuda:0")
+    dvl.probe_mfma(False, 5, sink)
+    torch.cuda.synchronize()
+    assert torch.all(sink == 32 * 4 * 32 * 5)
+    sink.fill_(float("nan"))
+    dvl.probe_mfma(True, 5, sink)
+    torch.cuda.synchronize()
+    assert torch.all(torch.isfinite(sink))
