@@ -57,14 +57,19 @@ __global__ __launch_bounds__(C::NT) void k_down_partial(const typename C::elem* 
   }
 }
 
+// Four consecutive elements per thread (n is a multiple of 4: r % 16 == 0); the loop over the
+// splits is unrolled so that several splits' loads are in flight at once. The sum runs over the
+// splits in order, so the result does not depend on the launch.
 template <typename T, int ACT>
 __global__ __launch_bounds__(256) void k_reduce_act(const float* __restrict__ part,
                                                     T* __restrict__ Z, int64_t n, int splits) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= n) return;
-  float x = 0.f;
-  for (int s = 0; s < splits; ++s) x += part[(int64_t)s * n + i];
-  Z[i] = from_f32<T>(ACT == 0 ? silu(x) : gelu(x));
+  f32x4 x = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int s = 0; s < splits; ++s) x += *(const f32x4*)(part + (int64_t)s * n + i);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) Z[i + u] = from_f32<T>(ACT == 0 ? silu(x[u]) : gelu(x[u]));
 }
 
 // M_l = Min + Z_l U_l. Min is E (layer 0, call dtype) or the fp32 state (it may alias Mst).
@@ -353,9 +358,9 @@ static hipError_t rec_launch(const void* E, const void* Dw, const void* Uw, cons
       k_down_partial<C><<<gd, dim3(C::NT), C::LDS_BYTES, s>>>(X, (const T*)Dw + (int64_t)l * r * d,
                                                               part, T_, d, r, kchunk);
     if (act == 0)
-      k_reduce_act<T, 0><<<rcdiv(nz, 256), 256, 0, s>>>(part, Z, nz, w.splits);
+      k_reduce_act<T, 0><<<rcdiv(nz / 4, 256), 256, 0, s>>>(part, Z, nz, w.splits);
     else
-      k_reduce_act<T, 1><<<rcdiv(nz, 256), 256, 0, s>>>(part, Z, nz, w.splits);
+      k_reduce_act<T, 1><<<rcdiv(nz / 4, 256), 256, 0, s>>>(part, Z, nz, w.splits);
     const T* Ul = (const T*)Uw + (int64_t)l * d * r;
     const T* gl = (const T*)gamma + (int64_t)l * d;
     T* Mgl = Mg + (int64_t)l * T_ * d;
