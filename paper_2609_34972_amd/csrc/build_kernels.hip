@@ -274,17 +274,23 @@ __global__ __launch_bounds__(C::NT) void k_down_act_p(const bf16* __restrict__ E
   }
 }
 
-// Up-projection epilogue staging: the fp32 tile, rows padded by 4 floats so the transposed
-// accumulator writes (32 rows at one column per instruction) hit distinct banks.
-template <class C>
-constexpr int up_lds_bytes() {
-  return C::BM * (C::BN + 4) * 4 > C::LDS_BYTES ? C::BM * (C::BN + 4) * 4 : C::LDS_BYTES;
-}
-constexpr int kUpLdsBytes = up_lds_bytes<UpP>();
+// Up-projection epilogue scratch past the two stages: per wave a 16 x 64 bf16 transpose buffer
+// (rows padded by 16 bytes), then the per-row sums of squares of the two column halves.
+constexpr int kUpScrPitch = UpP::WN + 8;  // bf16 elements
+constexpr int kUpScrOffset = UpP::LDS_BYTES;
+constexpr int kUpSsOffset = kUpScrOffset + UpP::NWAVES * 16 * kUpScrPitch * 2;
+constexpr int kUpLdsBytes = kUpSsOffset + UpP::WGN * UpP::BM * 4;
 
 // Layers per block of the up projection: the block's tile of E is read once for all of them.
 constexpr int kUpLayers = 4;
 
+// One 128 x 128 tile of M_l * gamma_l for kUpLayers consecutive layers through one pipeline
+// (the next layer's first operand tiles load while a layer's epilogue runs). The epilogue works
+// on the accumulators in place: lane l holds row l % 16 of each 16-row fragment and four
+// consecutive columns, E and gamma are fetched in that layout, the per-row sum of squares of fp32
+// M is a shuffle over the four lanes of a row plus one LDS exchange between the two waves of a
+// row band, and each wave turns its bf16 rows around through a 2 KiB LDS buffer so that they
+// leave as whole 128-byte lines.
 template <class C>
 __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        const bf16* __restrict__ Z,
@@ -293,83 +299,104 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        bf16* __restrict__ Mg,
                                                        float* __restrict__ ssq, int T, int d,
                                                        int r, int l0, int nl) {
+  static_assert(C::WGN == 2 && C::WN == 64, "epilogue assumes two 64-column wave halves");
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int kUpPitch = C::BN + 4;
   const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
-  const int lz_begin = blockIdx.z * kUpLayers, lz_end = min(nl, lz_begin + kUpLayers);
+  const int lz0 = blockIdx.z * kUpLayers, nrun = min(nl - lz0, kUpLayers);
   const int ldb = r * 2;
-  // The epilogue's rows of E (16 lanes x 16 bytes per 128-column row, BM/16 rows per thread)
-  // are fetched once, before the first main loop, and serve every layer of the block.
-  constexpr int kRows = C::BM / (C::NT / 16);
-  const int c8 = (threadIdx.x & 15) * 8;
-  const int r16 = threadIdx.x >> 4;
-  const bool col_ok = n0 + c8 < d;  // d is a multiple of 64, so a chunk is all in or all out
-  u32x4 e_pre[kRows];
-#pragma unroll
-  for (int i = 0; i < kRows; ++i) {
-    const int row = m0 + r16 + i * (C::NT / 16);
-    e_pre[i] = (row < T && col_ok) ? *(const u32x4*)(E + (int64_t)row * d + n0 + c8) : u32x4{};
-  }
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int row0 = m0 + wm * C::WM + pipe_row(lane);       // + a * 16
+  const int col0 = n0 + wn * C::WN + pipe_col(lane);       // + b * 16
+  const bool cols_ok = n0 + wn * C::WN < d;  // d % 64 == 0: a wave's 64 columns are all in or out
+  // E in the accumulator layout, fetched once for every layer of the block.
+  u32x2 e4[C::FM][C::FN];
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b)
+      e4[a][b] = (cols_ok && row0 + a * 16 < T)
+                     ? *(const u32x2*)(E + (int64_t)(row0 + a * 16) * d + col0 + b * 16)
+                     : u32x2{};
+  auto load_gamma = [&](int lz, u32x2 (&g)[C::FN]) {
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b)
+      g[b] = cols_ok ? *(const u32x2*)(gamma + (int64_t)(l0 + lz) * d + col0 + b * 16) : u32x2{};
+  };
+  u32x2 g4[C::FN];
+  load_gamma(lz0, g4);
+  bf16* scr = (bf16*)(smem + kUpScrOffset) + wave * 16 * kUpScrPitch;
+  float* ssx = (float*)(smem + kUpSsOffset);
   const int np = (d + C::BN - 1) / C::BN;
-  float* tile = (float*)smem;
-  for (int lz = lz_begin; lz < lz_end; ++lz) {
-    const int l = l0 + lz;
+
+  auto operands = [&](int run, BufOperand& A, BufOperand& B) {
+    const int l = l0 + lz0 + run;
     const bf16* Zl = Z + (int64_t)l * T * r;
     const bf16* Ul = Uw + (int64_t)l * d * r;
-    BufOperand A{buffer_rsrc(Zl + (int64_t)m0 * r, (int64_t)(T - m0) * ldb), buffer_rsrc(Zl, 0),
-                 1 << 30, ldb};
-    BufOperand B{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
-                 1 << 30, ldb};
-    bf16x8 g8 = {};
-    if (col_ok) g8 = __builtin_bit_cast(bf16x8, *(const u32x4*)(gamma + (int64_t)l * d + n0 + c8));
-    f32x4 acc[C::FM][C::FN];
-    // Its first wait also covers the previous layer's stores, which precede its loads.
-    pipe_mainloop<C>(A, B, r, (bf16*)smem, acc);
-
-    // 1. Z_l U_l tile (fp32) into LDS. The main loop's last LDS read precedes its last barrier.
+    A = BufOperand{buffer_rsrc(Zl + (int64_t)m0 * r, (int64_t)(T - m0) * ldb), buffer_rsrc(Zl, 0),
+                   1 << 30, ldb};
+    B = BufOperand{buffer_rsrc(Ul + (int64_t)n0 * r, (int64_t)(d - n0) * ldb), buffer_rsrc(Ul, 0),
+                   1 << 30, ldb};
+  };
+  auto epilogue = [&](int run, f32x4 (&acc)[C::FM][C::FN]) {
+    const int lz = lz0 + run;
+    bf16* Ml = Mg + (int64_t)lz * T * d;
+    float ssr[C::FM];
 #pragma unroll
     for (int a = 0; a < C::FM; ++a) {
-      const int rl = wm * C::WM + a * 16 + pipe_row(lane);
-#pragma unroll
-      for (int b = 0; b < C::FN; ++b)
-        *(f32x4*)(tile + rl * kUpPitch + wn * C::WN + b * 16 + pipe_col(lane)) = acc[a][b];
-    }
-    __syncthreads();
-    // 2. Rows of the tile: 16 lanes x 8 columns each cover the 128 columns, so E, gamma and the
-    //    output move as whole 16-byte pieces of a row, and the row's sum of squares over this
-    //    column tile is a 16-lane shuffle.
-    bf16* Ml = Mg + (int64_t)lz * T * d;
-#pragma unroll
-    for (int i = 0; i < kRows; ++i) {
-      const int rr = r16 + i * (C::NT / 16);
-      const int row = m0 + rr;
       float ss = 0.f;
-      if (row < T && col_ok) {
-        const bf16x8 e8 = __builtin_bit_cast(bf16x8, e_pre[i]);
-        const f32x4 p0 = *(const f32x4*)(tile + rr * kUpPitch + c8);
-        const f32x4 p1 = *(const f32x4*)(tile + rr * kUpPitch + c8 + 4);
-        bf16x8 o;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const float m = (u < 4 ? p0[u] : p1[u - 4]) + (float)e8[u];
+      for (int b = 0; b < C::FN; ++b) {
+        const bf16x4 e = __builtin_bit_cast(bf16x4, e4[a][b]);
+        const bf16x4 g = __builtin_bit_cast(bf16x4, g4[b]);
+        bf16x4 o;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float m = acc[a][b][u] + (float)e[u];
           ss += m * m;
-          o[u] = (bf16)(m * (float)g8[u]);
+          o[u] = (bf16)(m * (float)g[u]);
         }
+        *(u32x2*)(scr + pipe_row(lane) * kUpScrPitch + b * 16 + pipe_col(lane)) =
+            __builtin_bit_cast(u32x2, o);
+      }
+      ss += shfl_xor(ss, 16);
+      ss += shfl_xor(ss, 32);
+      ssr[a] = ss;
+      // The buffer is this wave's own: LDS serves a wave's accesses in order, so a wave-level
+      // fence is all the read-back needs.
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int rr = h * 8 + (lane >> 3);
+        const u32x4 v = *(const u32x4*)(scr + rr * kUpScrPitch + (lane & 7) * 8);
+        const int row = m0 + wm * C::WM + a * 16 + rr;
         // Streaming store: M * gamma of all layers (0.6 GB at LLaVA-7B shapes) is read only by
         // the projection launch; through the caches the stores ran at about 1.8 TB/s.
-        __builtin_nontemporal_store(__builtin_bit_cast(u32x4, o),
-                                    (u32x4*)(Ml + (int64_t)row * d + n0 + c8));
+        if (cols_ok && row < T)
+          __builtin_nontemporal_store(
+              v, (u32x4*)(Ml + (int64_t)row * d + n0 + wn * C::WN + (lane & 7) * 8));
       }
-      ss += shfl_xor(ss, 1);
-      ss += shfl_xor(ss, 2);
-      ss += shfl_xor(ss, 4);
-      ss += shfl_xor(ss, 8);
-      if ((threadIdx.x & 15) == 0 && row < T) ssq[((int64_t)lz * np + blockIdx.x) * T + row] = ss;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    __syncthreads();  // the staging tile is read before the next layer's loads overwrite it
-  }
+    if (run + 1 < nrun) load_gamma(lz + 1, g4);
+    // Row sums of the two column halves meet in LDS. The previous layer's exchange was read
+    // before at least one barrier of this layer's main loop.
+    if (lane < 16) {
+#pragma unroll
+      for (int a = 0; a < C::FM; ++a) ssx[wn * C::BM + wm * C::WM + a * 16 + lane] = ssr[a];
+    }
+    pipe_sync<waitcnt_imm(63, 0)>();  // LDS writes done; the stores stay in flight
+    if (threadIdx.x < C::BM) {
+      const int row = m0 + threadIdx.x;
+      if (row < T)
+        ssq[((int64_t)lz * np + blockIdx.x) * T + row] = ssx[threadIdx.x] + ssx[C::BM + threadIdx.x];
+    }
+  };
+  pipe_runs<C>(nrun, r, (bf16*)smem, operands, epilogue);
 }
 
 // Backbone epilogue arguments as the kernels see them (see KvEpiArgs).

@@ -185,4 +185,68 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
   }
 }
 
+// Several GEMMs of the same K through one pipeline (e.g. one output tile of consecutive layers).
+// Tile t of the stream is K tile t % nk of run t / nk, nk = K / 64. operands(run, A, B) fills a
+// run's operands (every run has the same row pitches); epilogue(run, acc) consumes a finished
+// run while the loads of the next run's first two tiles are in flight, so the pipeline does not
+// drain between runs. The epilogue may use LDS past the two stages (C::LDS_BYTES) but not the
+// stages themselves, since a landed tile may sit there.
+template <class C, class Operands, class Epilogue>
+__device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands operands,
+                                          Epilogue epilogue) {
+  f32x4 acc[C::FM][C::FN];
+#pragma unroll
+  for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+    for (int b = 0; b < C::FN; ++b) acc[a][b] = f32x4{};
+  const int nk = K / C::BK, nt = nruns * nk;
+  BufOperand A, B;
+  operands(0, A, B);
+  const int va0 = pipe_lane_offset(A.ld_bytes, 0), va1 = pipe_lane_offset(A.ld_bytes, 1);
+  const int vb0 = pipe_lane_offset(B.ld_bytes, 0), vb1 = pipe_lane_offset(B.ld_bytes, 1);
+  auto issue = [&](int t, bf16* stage) {
+    const int run = t / nk;
+    BufOperand a, b;
+    operands(run, a, b);
+    pipe_issue<C>(a, b, (t - run * nk) * C::BK * 2, stage, va0, va1, vb0, vb1);
+  };
+  issue(0, lds);
+  if (nt > 1) {
+    issue(1, lds + C::STAGE);
+    pipe_sync<waitcnt_imm(C::INS, 0)>();
+  } else {
+    pipe_sync<waitcnt_imm(0, 0)>();
+  }
+  bf16x8 fa[2][C::FM], fb[2][C::FN];
+  pipe_frags<C>(lds, 0, fa[0], fb[0]);
+  int kk = 0, run = 0;  // K tile of t within its run, and its run
+  for (int t = 0; t < nt; ++t) {
+    bf16* s = lds + (t & 1) * C::STAGE;
+    pipe_frags<C>(s, 1, fa[1], fb[1]);
+    pipe_mfmas<C>(acc, fa[0], fb[0]);
+    constexpr int kLead = (C::FM * C::FN - 2 * (C::FM + C::FN)) / 2;
+    static_assert(kLead >= 0, "a K step needs two MFMAs per fragment read");
+    __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
+#pragma unroll
+    for (int i = 0; i < C::FM + C::FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kLead - 2 * (C::FM + C::FN), 0);
+    pipe_sync<waitcnt_imm(0, 0)>();
+    if (t + 2 < nt) issue(t + 2, s);
+    if (t + 1 < nt) pipe_frags<C>(lds + ((t + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
+    pipe_mfmas<C>(acc, fa[1], fb[1]);
+    if (++kk == nk) {
+      epilogue(run, acc);
+#pragma unroll
+      for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+        for (int b = 0; b < C::FN; ++b) acc[a][b] = f32x4{};
+      kk = 0;
+      ++run;
+    }
+  }
+}
+
 }  // namespace dv
