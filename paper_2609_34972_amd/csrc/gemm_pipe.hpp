@@ -75,26 +75,56 @@ __device__ __forceinline__ int pipe_lane_offset(int ld_bytes, int odd_block) {
   return r * ld_bytes + ((pc ^ key) << 4);
 }
 
+// What a wave's refill loads need besides the K offset, fixed for a whole GEMM: the buffer of
+// each B load (the B tile may straddle the two row ranges) and the byte offset of each load's
+// 8-row block. Worked out once, so a refill costs one scalar add per load.
+struct PipeRsrc {  // (an array of the bare resource type does not compile for the host pass)
+  __amdgpu_buffer_rsrc_t r;
+};
 template <class C>
-__device__ __forceinline__ void pipe_issue(const BufOperand& A, const BufOperand& B, int kbytes,
-                                           bf16* stage, int va0, int va1, int vb0, int vb1) {
+struct PipeLoads {
+  __amdgpu_buffer_rsrc_t ra;
+  PipeRsrc rb[C::B_INS];
+  int sa[C::A_INS], sb[C::B_INS];
+};
+
+template <class C>
+__device__ __forceinline__ PipeLoads<C> pipe_loads(const BufOperand& A, const BufOperand& B) {
+  PipeLoads<C> p;
+  const int wave = wave_index();
+  p.ra = A.r0;
+#pragma unroll
+  for (int i = 0; i < C::A_INS; ++i) p.sa[i] = (wave * C::A_INS + i) * 8 * A.ld_bytes;
+#pragma unroll
+  for (int i = 0; i < C::B_INS; ++i) {
+    const int row = (wave * C::B_INS + i) * 8;
+    const bool first = row < B.nsplit;
+    p.rb[i].r = first ? B.r0 : B.r1;
+    p.sb[i] = (first ? row : row - B.nsplit) * B.ld_bytes;
+  }
+  return p;
+}
+
+// Each wave issues A_INS + B_INS 1 KiB loads (8 rows x 128 bytes) of one 64-deep K tile. With
+// an even count per wave, a load's block parity (which selects the swizzle key half) is that of
+// its index.
+template <class C>
+__device__ __forceinline__ void pipe_issue(const PipeLoads<C>& p, int kbytes, bf16* stage, int va0,
+                                           int va1, int vb0, int vb1) {
+  static_assert(C::A_INS % 2 == 0 && C::B_INS % 2 == 0, "block parity must follow the index");
   const int wave = wave_index();
 #pragma unroll
   for (int i = 0; i < C::A_INS; ++i) {
     const int blk = wave * C::A_INS + i;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(A.r0, (lds_void*)(stage + blk * 512), 16,
-                                             (blk & 1) ? va1 : va0, blk * 8 * A.ld_bytes + kbytes,
-                                             0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(p.ra, (lds_void*)(stage + blk * 512), 16,
+                                             (i & 1) ? va1 : va0, p.sa[i] + kbytes, 0, 0);
   }
   bf16* sb = stage + C::BM * C::BK;
 #pragma unroll
   for (int i = 0; i < C::B_INS; ++i) {
     const int blk = wave * C::B_INS + i;
-    const int row = blk * 8;
-    const bool first = row < B.nsplit;
-    const int soff = (first ? row : row - B.nsplit) * B.ld_bytes + kbytes;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(first ? B.r0 : B.r1, (lds_void*)(sb + blk * 512), 16,
-                                             (blk & 1) ? vb1 : vb0, soff, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(p.rb[i].r, (lds_void*)(sb + blk * 512), 16,
+                                             (i & 1) ? vb1 : vb0, p.sb[i] + kbytes, 0, 0);
   }
 }
 
@@ -152,9 +182,10 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
   const int va0 = pipe_lane_offset(A.ld_bytes, 0), va1 = pipe_lane_offset(A.ld_bytes, 1);
   const int vb0 = pipe_lane_offset(B.ld_bytes, 0), vb1 = pipe_lane_offset(B.ld_bytes, 1);
   const int nk = K / C::BK;
-  pipe_issue<C>(A, B, 0, lds, va0, va1, vb0, vb1);
+  const PipeLoads<C> pl = pipe_loads<C>(A, B);
+  pipe_issue<C>(pl, 0, lds, va0, va1, vb0, vb1);
   if (nk > 1) {
-    pipe_issue<C>(A, B, C::BK * 2, lds + C::STAGE, va0, va1, vb0, vb1);
+    pipe_issue<C>(pl, C::BK * 2, lds + C::STAGE, va0, va1, vb0, vb1);
     pipe_sync<waitcnt_imm(C::INS, 0)>();  // tile 0 landed, tile 1 stays in flight
   } else {
     pipe_sync<waitcnt_imm(0, 0)>();
@@ -179,9 +210,38 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
     // K step 1: every wave holds its last fragments of stage s and tile kt+1 has landed:
     // refill s with tile kt+2 and fetch tile kt+1's first fragments before this step's MFMAs.
     pipe_sync<waitcnt_imm(0, 0)>();
-    if (kt + 2 < nk) pipe_issue<C>(A, B, (kt + 2) * C::BK * 2, s, va0, va1, vb0, vb1);
+    if (kt + 2 < nk) pipe_issue<C>(pl, (kt + 2) * C::BK * 2, s, va0, va1, vb0, vb1);
     if (kt + 1 < nk) pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
     pipe_mfmas<C>(acc, fa[1], fb[1]);
+  }
+}
+
+// Refill loads of tile t of a run stream (K tile t % nk of run t / nk), with the per-load
+// offsets worked out at each call (a run's operands change from run to run).
+template <class C, class Operands>
+__device__ __forceinline__ void pipe_issue_run(Operands& operands, int t, int nk, bf16* stage,
+                                               int va0, int va1, int vb0, int vb1) {
+  const int run = t / nk;
+  BufOperand A, B;
+  operands(run, A, B);
+  const int kbytes = (t - run * nk) * C::BK * 2;
+  const int wave = wave_index();
+#pragma unroll
+  for (int i = 0; i < C::A_INS; ++i) {
+    const int blk = wave * C::A_INS + i;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(A.r0, (lds_void*)(stage + blk * 512), 16,
+                                             (blk & 1) ? va1 : va0, blk * 8 * A.ld_bytes + kbytes,
+                                             0, 0);
+  }
+  bf16* sb = stage + C::BM * C::BK;
+#pragma unroll
+  for (int i = 0; i < C::B_INS; ++i) {
+    const int blk = wave * C::B_INS + i;
+    const int row = blk * 8;
+    const bool first = row < B.nsplit;
+    const int soff = (first ? row : row - B.nsplit) * B.ld_bytes + kbytes;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(first ? B.r0 : B.r1, (lds_void*)(sb + blk * 512), 16,
+                                             (blk & 1) ? vb1 : vb0, soff, 0, 0);
   }
 }
 
@@ -204,15 +264,10 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
   operands(0, A, B);
   const int va0 = pipe_lane_offset(A.ld_bytes, 0), va1 = pipe_lane_offset(A.ld_bytes, 1);
   const int vb0 = pipe_lane_offset(B.ld_bytes, 0), vb1 = pipe_lane_offset(B.ld_bytes, 1);
-  auto issue = [&](int t, bf16* stage) {
-    const int run = t / nk;
-    BufOperand a, b;
-    operands(run, a, b);
-    pipe_issue<C>(a, b, (t - run * nk) * C::BK * 2, stage, va0, va1, vb0, vb1);
-  };
-  issue(0, lds);
+
+  pipe_issue_run<C>(operands, 0, nk, lds, va0, va1, vb0, vb1);
   if (nt > 1) {
-    issue(1, lds + C::STAGE);
+    pipe_issue_run<C>(operands, 1, nk, lds + C::STAGE, va0, va1, vb0, vb1);
     pipe_sync<waitcnt_imm(C::INS, 0)>();
   } else {
     pipe_sync<waitcnt_imm(0, 0)>();
@@ -234,7 +289,7 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
     }
     __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kLead - 2 * (C::FM + C::FN), 0);
     pipe_sync<waitcnt_imm(0, 0)>();
-    if (t + 2 < nt) issue(t + 2, s);
+    if (t + 2 < nt) pipe_issue_run<C>(operands, t + 2, nk, s, va0, va1, vb0, vb1);
     if (t + 1 < nt) pipe_frags<C>(lds + ((t + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
     pipe_mfmas<C>(acc, fa[1], fb[1]);
     if (++kk == nk) {
