@@ -5,7 +5,11 @@
 //   of faulting.
 // * Two 64-deep LDS stages: the loads of tile k+2 are issued as soon as every wave has finished
 //   reading tile k, and the next tile's first fragments are read before the last MFMA group of
-//   the current tile, so one barrier per K tile carries no exposed LDS latency.
+//   the current tile, so one barrier per K tile carries no exposed LDS latency. Both halves of a
+//   tile interleave their memory instructions with MFMAs: before the barrier the second K step's
+//   fragment reads, after it the refill loads and the next tile's first fragment reads.
+// * Out-of-range buffer loads fetch nothing and write zeros, also into LDS (measured on gfx950,
+//   whether the excess offset sits in the vector or the scalar offset).
 // * 128-byte LDS rows with an XOR swizzle of the 16-byte chunks keyed on (row / 2) mod 8: the
 //   16 rows read together by a fragment load land in 16 distinct bank groups. Lanes of a load
 //   instruction pick the global chunk that belongs at their LDS slot, so the swizzle costs
@@ -34,6 +38,9 @@ constexpr int waitcnt_imm(int vm, int lgkm) {
 }
 
 constexpr int kRawBufferFlags = 0x00020000;  // dword 3 of a raw (unformatted) buffer resource
+// A load offset past every operand buffer's range (they are at most 2^31 - 1 bytes and the
+// in-tile offsets stay far below 2^30): such a load fetches nothing and returns zeros.
+constexpr int kPipeOutOfRange = 0x40000000;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int64_t bytes) {
   const int nr = bytes > 0x7fffffff ? 0x7fffffff : (bytes < 0 ? 0 : (int)bytes);
@@ -207,13 +214,40 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kLead - 2 * (C::FM + C::FN), 0);
+    // Keep this step's MFMAs ahead of the barrier (the compiler would otherwise sink them below
+    // it, next to their next use), so they cover the fragment reads the barrier waits for.
+#pragma unroll
+    for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+      for (int b = 0; b < C::FN; ++b) asm volatile("" : "+v"(acc[a][b]));
     // K step 1: every wave holds its last fragments of stage s and tile kt+1 has landed:
     // refill s with tile kt+2 and fetch tile kt+1's first fragments before this step's MFMAs.
     pipe_sync<waitcnt_imm(0, 0)>();
-    if (kt + 2 < nk) pipe_issue<C>(pl, (kt + 2) * C::BK * 2, s, va0, va1, vb0, vb1);
-    if (kt + 1 < nk) pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
+    // Neither the refill nor the next fragment reads is conditional, so both interleave with
+    // this step's MFMAs: past the last tile the refill offset lies beyond the buffers' range
+    // (nothing is fetched; the stage, which is not read again, fills with zeros) and the
+    // fragments read from a stale stage go unused.
+    const int kb2 = kt + 2 < nk ? (kt + 2) * C::BK * 2 : kPipeOutOfRange;
+    pipe_issue<C>(pl, kb2, s, va0, va1, vb0, vb1);
+    pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
     pipe_mfmas<C>(acc, fa[1], fb[1]);
+#pragma unroll
+    for (int i = 0; i < C::INS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    }
+#pragma unroll
+    for (int i = 0; i < C::FM + C::FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - C::INS - (C::FM + C::FN), 1);
+    __builtin_amdgcn_sched_barrier(0);  // keeps the two K steps' patterns in separate regions
   }
+  // The last tile's zero-filling refill and fragment reads come after the last barrier: every
+  // wave's must be complete before any wave goes on to reuse the stages (epilogues may write
+  // them without a barrier of their own).
+  pipe_sync<waitcnt_imm(0, 0)>();
 }
 
 // Refill loads of tile t of a run stream (K tile t % nk of run t / nk), with the per-load
