@@ -241,6 +241,7 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
     }
+    static_assert(C::FM * C::FN >= C::INS + C::FM + C::FN, "one MFMA per load and per read");
     __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - C::INS - (C::FM + C::FN), 1);
     __builtin_amdgcn_sched_barrier(0);  // keeps the two K steps' patterns in separate regions
   }
@@ -252,13 +253,17 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
 
 // Refill loads of tile t of a run stream (K tile t % nk of run t / nk), with the per-load
 // offsets worked out at each call (a run's operands change from run to run).
+// A t at or past nt (the stream's end) issues out-of-range loads of the last run, which fetch
+// nothing and fill the stage with zeros.
 template <class C, class Operands>
-__device__ __forceinline__ void pipe_issue_run(Operands& operands, int t, int nk, bf16* stage,
-                                               int va0, int va1, int vb0, int vb1) {
-  const int run = t / nk;
+__device__ __forceinline__ void pipe_issue_run(Operands& operands, int t, int nk, int nt,
+                                               bf16* stage, int va0, int va1, int vb0, int vb1) {
+  const bool past = t >= nt;
+  const int tt = past ? nt - 1 : t;
+  const int run = tt / nk;
   BufOperand A, B;
   operands(run, A, B);
-  const int kbytes = (t - run * nk) * C::BK * 2;
+  const int kbytes = past ? kPipeOutOfRange : (tt - run * nk) * C::BK * 2;
   const int wave = wave_index();
 #pragma unroll
   for (int i = 0; i < C::A_INS; ++i) {
@@ -299,9 +304,9 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
   const int va0 = pipe_lane_offset(A.ld_bytes, 0), va1 = pipe_lane_offset(A.ld_bytes, 1);
   const int vb0 = pipe_lane_offset(B.ld_bytes, 0), vb1 = pipe_lane_offset(B.ld_bytes, 1);
 
-  pipe_issue_run<C>(operands, 0, nk, lds, va0, va1, vb0, vb1);
+  pipe_issue_run<C>(operands, 0, nk, nt, lds, va0, va1, vb0, vb1);
   if (nt > 1) {
-    pipe_issue_run<C>(operands, 1, nk, lds + C::STAGE, va0, va1, vb0, vb1);
+    pipe_issue_run<C>(operands, 1, nk, nt, lds + C::STAGE, va0, va1, vb0, vb1);
     pipe_sync<waitcnt_imm(C::INS, 0)>();
   } else {
     pipe_sync<waitcnt_imm(0, 0)>();
@@ -322,10 +327,27 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kLead - 2 * (C::FM + C::FN), 0);
+#pragma unroll
+    for (int a = 0; a < C::FM; ++a)
+#pragma unroll
+      for (int b = 0; b < C::FN; ++b) asm volatile("" : "+v"(acc[a][b]));
     pipe_sync<waitcnt_imm(0, 0)>();
-    if (t + 2 < nt) pipe_issue_run<C>(operands, t + 2, nk, s, va0, va1, vb0, vb1);
-    if (t + 1 < nt) pipe_frags<C>(lds + ((t + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
+    pipe_issue_run<C>(operands, t + 2, nk, nt, s, va0, va1, vb0, vb1);
+    pipe_frags<C>(lds + ((t + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
     pipe_mfmas<C>(acc, fa[1], fb[1]);
+#pragma unroll
+    for (int i = 0; i < C::INS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    }
+#pragma unroll
+    for (int i = 0; i < C::FM + C::FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    }
+    static_assert(C::FM * C::FN >= C::INS + C::FM + C::FN, "one MFMA per load and per read");
+    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - C::INS - (C::FM + C::FN), 1);
+    __builtin_amdgcn_sched_barrier(0);
     if (++kk == nk) {
       epilogue(run, acc);
 #pragma unroll
@@ -336,6 +358,7 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
       ++run;
     }
   }
+  pipe_sync<waitcnt_imm(0, 0)>();  // as at the end of pipe_mainloop
 }
 
 }  // namespace dv
