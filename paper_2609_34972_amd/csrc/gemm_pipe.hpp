@@ -178,6 +178,26 @@ __device__ __forceinline__ void pipe_sync() {
 __device__ __forceinline__ int pipe_row(int lane) { return lane & 15; }
 __device__ __forceinline__ int pipe_col(int lane) { return (lane >> 4) * 4; }
 
+// Issue order of the second K step: the refill loads first, each followed by kPer MFMAs (loads
+// spread out went slightly faster than one per MFMA; fragment reads first, slower), then each of
+// the next tile's fragment reads followed by one MFMA, then the rest of the MFMAs.
+template <class C>
+__device__ __forceinline__ void pipe_step1_pattern() {
+  constexpr int kPer = (C::FM * C::FN - (C::FM + C::FN)) / C::INS;
+  static_assert(kPer >= 1, "one MFMA per load and per read");
+#pragma unroll
+  for (int i = 0; i < C::INS; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
+    __builtin_amdgcn_sched_group_barrier(0x008, kPer, 1);
+  }
+#pragma unroll
+  for (int i = 0; i < C::FM + C::FN; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kPer * C::INS - (C::FM + C::FN), 1);
+}
+
 // A: block-tile rows start at A's first row; B likewise. K must be a multiple of 64.
 template <class C>
 __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOperand& B, int K,
@@ -231,18 +251,7 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
     pipe_issue<C>(pl, kb2, s, va0, va1, vb0, vb1);
     pipe_frags<C>(lds + ((kt + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
     pipe_mfmas<C>(acc, fa[1], fb[1]);
-#pragma unroll
-    for (int i = 0; i < C::INS; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-    }
-#pragma unroll
-    for (int i = 0; i < C::FM + C::FN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-    }
-    static_assert(C::FM * C::FN >= C::INS + C::FM + C::FN, "one MFMA per load and per read");
-    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - C::INS - (C::FM + C::FN), 1);
+    pipe_step1_pattern<C>();
     __builtin_amdgcn_sched_barrier(0);  // keeps the two K steps' patterns in separate regions
   }
   // The last tile's zero-filling refill and fragment reads come after the last barrier: every
@@ -335,18 +344,7 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
     pipe_issue_run<C>(operands, t + 2, nk, nt, s, va0, va1, vb0, vb1);
     pipe_frags<C>(lds + ((t + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
     pipe_mfmas<C>(acc, fa[1], fb[1]);
-#pragma unroll
-    for (int i = 0; i < C::INS; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-    }
-#pragma unroll
-    for (int i = 0; i < C::FM + C::FN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-    }
-    static_assert(C::FM * C::FN >= C::INS + C::FM + C::FN, "one MFMA per load and per read");
-    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - C::INS - (C::FM + C::FN), 1);
+    pipe_step1_pattern<C>();
     __builtin_amdgcn_sched_barrier(0);
     if (++kk == nk) {
       epilogue(run, acc);
