@@ -178,6 +178,21 @@ __device__ __forceinline__ void pipe_sync() {
 __device__ __forceinline__ int pipe_row(int lane) { return lane & 15; }
 __device__ __forceinline__ int pipe_col(int lane) { return (lane >> 4) * 4; }
 
+// Issue order of the first K step: two MFMAs, then each of the second step's fragment reads
+// followed by one MFMA, then the rest (the reads, which the tile barrier waits for, go out early;
+// two MFMAs per read, or reads from the first MFMA on, measured equal or slower).
+template <class C>
+__device__ __forceinline__ void pipe_step0_pattern() {
+  static_assert(C::FM * C::FN >= 2 + C::FM + C::FN, "a K step needs an MFMA per fragment read");
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+#pragma unroll
+  for (int i = 0; i < C::FM + C::FN; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - 2 - (C::FM + C::FN), 0);
+}
+
 // Issue order of the second K step: the refill loads first, each followed by kPer MFMAs (loads
 // spread out went slightly faster than one per MFMA; fragment reads first, slower), then each of
 // the next tile's fragment reads followed by one MFMA, then the rest of the MFMAs.
@@ -221,19 +236,11 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
   pipe_frags<C>(lds, 0, fa[0], fb[0]);
   for (int kt = 0; kt < nk; ++kt) {
     bf16* s = lds + (kt & 1) * C::STAGE;
-    // K step 0: the step-1 fragments are read between its MFMAs (issue order: a few MFMAs,
-    // then each fragment read followed by two MFMAs, so the reads overlap the matrix pipe).
+    // K step 0: the step-1 fragments are read between its MFMAs (pipe_step0_pattern), so the
+    // reads overlap the matrix pipe.
     pipe_frags<C>(s, 1, fa[1], fb[1]);
     pipe_mfmas<C>(acc, fa[0], fb[0]);
-    constexpr int kLead = (C::FM * C::FN - 2 * (C::FM + C::FN)) / 2;
-    static_assert(kLead >= 0, "a K step needs two MFMAs per fragment read");
-    __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
-#pragma unroll
-    for (int i = 0; i < C::FM + C::FN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kLead - 2 * (C::FM + C::FN), 0);
+    pipe_step0_pattern<C>();
     // Keep this step's MFMAs ahead of the barrier (the compiler would otherwise sink them below
     // it, next to their next use), so they cover the fragment reads the barrier waits for.
 #pragma unroll
@@ -327,15 +334,7 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
     bf16* s = lds + (t & 1) * C::STAGE;
     pipe_frags<C>(s, 1, fa[1], fb[1]);
     pipe_mfmas<C>(acc, fa[0], fb[0]);
-    constexpr int kLead = (C::FM * C::FN - 2 * (C::FM + C::FN)) / 2;
-    static_assert(kLead >= 0, "a K step needs two MFMAs per fragment read");
-    __builtin_amdgcn_sched_group_barrier(0x008, kLead, 0);
-#pragma unroll
-    for (int i = 0; i < C::FM + C::FN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kLead - 2 * (C::FM + C::FN), 0);
+    pipe_step0_pattern<C>();
 #pragma unroll
     for (int a = 0; a < C::FM; ++a)
 #pragma unroll
