@@ -594,8 +594,8 @@ def run_decode(args, w, layers_timed=None):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported by this build "
-              "(the path runs on a single MI355X; see the sharding notes in the design document)",
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported (the kernels "
+              "run on a single MI355X; multi-GPU sharding is a design note, not an implemented path)",
               file=sys.stderr)
         sys.exit(2)
     import torch
