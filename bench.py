@@ -80,6 +80,9 @@ def parse():
                    help="skip the decode-shape measurement appended to prefill workloads")
     p.add_argument("--no-cold", action="store_true",
                    help="skip the cold-cache steps (512 MiB rewritten before each)")
+    p.add_argument("--no-workloads", action="store_true",
+                   help="skip the compact LLaVA-NeXT and Qwen2.5-VL video blocks appended to the "
+                        "default LLaVA-7B run")
     p.add_argument("--no-delta", action="store_true",
                    help="skip the linear-attention visual write appended to prefill workloads")
     p.add_argument("--no-variants", action="store_true",
@@ -121,6 +124,35 @@ def stored_traffic():
         return float(kv["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def provenance():
+    """Which sources produced the numbers: the git revision the library was built at (recorded
+    by the build, since runs may happen where no git metadata exists), whether that tree had
+    uncommitted changes, and a digest of the library sources as they are now."""
+    from paper_2609_34972_amd import build as hip_build
+    info = {}
+    try:
+        with open(hip_build.INFO) as f:
+            info = json.load(f)
+    except (OSError, ValueError):
+        pass
+    now = hip_build.sources_digest()
+    return {"git_rev": info.get("git_rev"), "git_dirty_at_build": info.get("git_dirty"),
+            "sources_sha256_16": now,
+            "library_built_from_these_sources": info.get("sources_sha256_16") == now,
+            "cpu_model": cpu_model(), "host_threads": os.cpu_count()}
 
 
 def percentiles(xs):
@@ -182,15 +214,20 @@ def cpu_baseline(w, E, wts, tx, vcache):
                                      f64(tx["Vt"][0][b:b + 1, g:g + 1]), w.q_pos0)
     t_attn = (time.perf_counter() - t0) / groups * (w.B * w.Hkv) * w.L
     t_step = build_per_token * w.T + t_attn
+    f_build = w.T / tok * w.L / nl
+    f_attn = w.B * w.Hkv * w.L / groups
     return {
         "value": w.T / t_step,
         "unit": "visual tokens/s",
         "cores": threads,
         "kind": "oracle",
+        "cpu_model": cpu_model(),
+        "scale_build": f_build,
+        "scale_attention": f_attn,
         "sample": (f"fp64 oracle: build+KV of {tok} tokens x {nl} of {w.L} layers "
-                   f"({t_build:.2f} s, scaled x{w.T / tok * w.L / nl:.0f}); attention of "
-                   f"{groups} (batch, kv-head) groups of one layer ({t_attn / (w.B * w.Hkv * w.L) * groups:.2f} s, "
-                   f"scaled x{w.B * w.Hkv * w.L / groups:.0f}); whole step {t_step:.1f} s"),
+                   f"({t_build:.2f} s, scaled x{f_build:.4g}); attention of "
+                   f"{groups} (batch, kv-head) groups of one layer ({t_attn / f_attn:.2f} s, "
+                   f"scaled x{f_attn:.4g}); whole step {t_step:.1f} s"),
     }
 
 
@@ -218,11 +255,133 @@ def mfma_probe(iters=2048, reps=3):
     return out
 
 
-def run_prefill(args, w):
+def alloc_step(w, Eg, tg):
+    """Outputs and workspaces of one step (all layers projected in one call)."""
     import torch
 
     import paper_2609_34972_amd as dvl
-    from paper_2609_34972_amd import configs, synth
+
+    dev, dt = Eg.device, Eg.dtype
+    buf = {
+        "Z": torch.empty(w.L, w.T, w.r, dtype=dt, device=dev),
+        "Kv": torch.empty(w.L, w.B, w.Hkv, w.Nv, w.hd, dtype=dt, device=dev),
+        "O": torch.empty_like(tg["Q"]),
+        "ws_kv": torch.empty(dvl.project_visual_kv_workspace(w.T, w.d, w.L, dt), dtype=torch.uint8,
+                             device=dev),
+    }
+    buf["Vv"] = torch.empty_like(buf["Kv"])
+    na = dvl.text_visual_attention_workspace(w.B, w.Hq, w.Hkv, w.hd, w.Nv, w.Nq, w.Nkt)
+    buf["ws_at"] = torch.empty(max(na, 16), dtype=torch.uint8, device=dev)
+    return buf
+
+
+def make_step(w, Eg, wg, tg, buf):
+    """One pass of the whole path: the all-layer down projection, the memories + norm + K/V of
+    every layer, and the attention of every layer. `ev` brackets the three build launches with
+    HIP events, `attn_ev` every attention launch."""
+    import paper_2609_34972_amd as dvl
+
+    Z, Kv, Vv, O = buf["Z"], buf["Kv"], buf["Vv"], buf["O"]
+
+    def step(ev=None, attn_ev=None):
+        if ev is not None:
+            dvl.time_kernel(dvl.KERNEL_DOWN, *ev["down"])
+            dvl.time_kernel(dvl.KERNEL_UP, *ev["up"])
+            dvl.time_kernel(dvl.KERNEL_KV, *ev["kv"])
+        dvl.build_visual_memory(Eg, wg["Dw"], Z, act=w.act)
+        dvl.project_visual_kv(Eg, Z, wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv, Vv, eps=w.eps,
+                              ws=buf["ws_kv"])
+        if ev is not None:
+            for k in (dvl.KERNEL_DOWN, dvl.KERNEL_UP, dvl.KERNEL_KV):
+                dvl.time_kernel(k)
+        for l in range(w.L):
+            if attn_ev is not None:
+                dvl.time_kernel(dvl.KERNEL_ATTENTION, *attn_ev[l])
+            dvl.text_visual_attention(tg["Q"][l], Kv[l], Vv[l], tg["Kt"][l], tg["Vt"][l], O[l],
+                                      q_pos0=w.q_pos0, ws=buf["ws_at"])
+        if attn_ev is not None:
+            dvl.time_kernel(dvl.KERNEL_ATTENTION)
+
+    return step
+
+
+def measure_step(w, step, steps, warmup, n_attn_steps=3):
+    """Time `steps` whole steps (the three build launches bracketed by HIP events inside the
+    timed region), then time the attention launches in `n_attn_steps` extra steps: events
+    between the 32 short attention launches would add gaps to the timed steps."""
+    import torch
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    hev = HipEvents()
+    evs = [{"down": hev.pair(), "up": hev.pair(), "kv": hev.pair()} for _ in range(steps)]
+    attn_evs = [[hev.pair() for _ in range(w.L)] for _ in range(n_attn_steps)]
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    t_begin, t_end = mk(), mk()
+    marks = [mk() for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t_begin.record()
+    for s in range(steps):
+        marks[s].record()
+        step(evs[s])
+    marks[-1].record()
+    t_end.record()
+    torch.cuda.synchronize()
+    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(steps)]
+    for s in range(n_attn_steps):
+        step(attn_ev=attn_evs[s])
+    torch.cuda.synchronize()
+    avg = lambda key: sum(hev.ms(e[key]) for e in evs) / steps
+    m = {"ms_step": t_begin.elapsed_time(t_end) / steps, "step_ms": step_ms,
+         "down": avg("down"), "up": avg("up"), "kv": avg("kv"),
+         "attn_launch": sum(hev.ms(a) for e in attn_evs for a in e) / (n_attn_steps * w.L)}
+    hev.close()
+    return m
+
+
+def step_figures(w, m, peak):
+    """Per-stage rates of a measured step against their bounds."""
+    from paper_2609_34972_amd import configs
+
+    f_down = 2.0 * w.T * w.d * w.r * w.L
+    f_up = 2.0 * w.T * w.r * w.d * w.L
+    f_kv = 2.0 * w.T * 2 * w.kv * w.d * w.L
+    f_build = f_down + f_up + f_kv
+    f_attn = configs.flops_attention(w)
+    b_attn = configs.bytes_attention(w)
+    ms_build = m["down"] + m["up"] + m["kv"]
+    ms_attn_total = m["ms_step"] - ms_build
+    ms_al = m["attn_launch"]
+    return {
+        "f_kv": f_kv, "f_build": f_build, "f_attn": f_attn,
+        "kv_tflops": f_kv / (m["kv"] * 1e-3) / 1e12,
+        "stages": {
+            "build_kv_visual_tokens_per_s": w.T / (ms_build * 1e-3),
+            "build_kv_ms": ms_build,
+            "build_kv_tflops": f_build / (ms_build * 1e-3) / 1e12,
+            "build_kv_mfma_frac": f_build / (ms_build * 1e-3) / 1e12 / peak,
+            "down_ms": m["down"], "up_ms": m["up"], "kv_ms": m["kv"],
+            "down_mfma_frac": f_down / (m["down"] * 1e-3) / 1e12 / peak,
+            "up_mfma_frac": f_up / (m["up"] * 1e-3) / 1e12 / peak,
+            "kv_mfma_frac": f_kv / (m["kv"] * 1e-3) / 1e12 / peak,
+            "attention_ms_all_layers": ms_attn_total,
+            "attention_kernel_ms_per_layer": ms_al,
+            "attention_tflops": f_attn / (ms_attn_total * 1e-3) / 1e12,
+            "attention_gbs": b_attn / (ms_attn_total * 1e-3) / 1e9,
+            "attention_hbm_frac": b_attn / (ms_attn_total * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "attention_kernel_gbs": b_attn / w.L / (ms_al * 1e-3) / 1e9,
+            "attention_kernel_hbm_frac": b_attn / w.L / (ms_al * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "attention_kernel_mfma_frac": f_attn / w.L / (ms_al * 1e-3) / 1e12 / peak,
+            "step_mfma_frac": (f_build + f_attn) / (m["ms_step"] * 1e-3) / 1e12 / peak,
+        },
+    }
+
+
+def run_prefill(args, w):
+    import torch
+
+    from paper_2609_34972_amd import synth
 
     dev = torch.device("cuda:0")
     log(f"[bench] generating {w.name} inputs")
@@ -232,80 +391,13 @@ def run_prefill(args, w):
     Eg = E.to(dev)
     wg = {k: v.to(dev) for k, v in wts.items()}
     tg = {k: v.to(dev) for k, v in tx.items()}
-    dt = Eg.dtype
-    Z = torch.empty(w.L, w.T, w.r, dtype=dt, device=dev)
-    Kv = torch.empty(w.L, w.B, w.Hkv, w.Nv, w.hd, dtype=dt, device=dev)
-    Vv = torch.empty_like(Kv)
-    O = torch.empty_like(tg["Q"])
-    ws_kv = torch.empty(dvl.project_visual_kv_workspace(w.T, w.d, w.L, dt), dtype=torch.uint8,
-                        device=dev)
-    na = dvl.text_visual_attention_workspace(w.B, w.Hq, w.Hkv, w.hd, w.Nv, w.Nq, w.Nkt)
-    ws_at = torch.empty(max(na, 16), dtype=torch.uint8, device=dev)
-
-    def step(ev=None, attn_ev=None):
-        if ev is not None:
-            dvl.time_kernel(dvl.KERNEL_DOWN, *ev["down"])
-            dvl.time_kernel(dvl.KERNEL_UP, *ev["up"])
-            dvl.time_kernel(dvl.KERNEL_KV, *ev["kv"])
-        dvl.build_visual_memory(Eg, wg["Dw"], Z, act=w.act)
-        dvl.project_visual_kv(Eg, Z, wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv, Vv, eps=w.eps,
-                              ws=ws_kv)
-        if ev is not None:
-            for k in (dvl.KERNEL_DOWN, dvl.KERNEL_UP, dvl.KERNEL_KV):
-                dvl.time_kernel(k)
-        for l in range(w.L):
-            if attn_ev is not None:
-                dvl.time_kernel(dvl.KERNEL_ATTENTION, *attn_ev[l])
-            dvl.text_visual_attention(tg["Q"][l], Kv[l], Vv[l], tg["Kt"][l], tg["Vt"][l], O[l],
-                                      q_pos0=w.q_pos0, ws=ws_at)
-        if attn_ev is not None:
-            dvl.time_kernel(dvl.KERNEL_ATTENTION)
-
-    log(f"[bench] warmup {args.warmup}")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # The timed steps bracket the three build launches with HIP events (the K/V projection is the
-    # roofline kernel). The 32 short attention launches are timed per kernel in separate steps
-    # after the timed region: events between them would add gaps to the measured step.
-    hev = HipEvents()
-    evs = [{"down": hev.pair(), "up": hev.pair(), "kv": hev.pair()} for _ in range(args.steps)]
-    n_attn_steps = 3
-    attn_evs = [[hev.pair() for _ in range(w.L)] for _ in range(n_attn_steps)]
-    mk = lambda: torch.cuda.Event(enable_timing=True)
-    t_begin, t_end = mk(), mk()
-    marks = [mk() for _ in range(args.steps + 1)]
-    log(f"[bench] timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t_begin.record()
-    for s in range(args.steps):
-        marks[s].record()
-        step(evs[s])
-    marks[-1].record()
-    t_end.record()
-    torch.cuda.synchronize()
-    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
-    for s in range(n_attn_steps):
-        step(attn_ev=attn_evs[s])
-    torch.cuda.synchronize()
-    ms_total = t_begin.elapsed_time(t_end)
-    ms_step = ms_total / args.steps
-    avg = lambda key: sum(hev.ms(e[key]) for e in evs) / args.steps
-    ms_down, ms_up, ms_kv = avg("down"), avg("up"), avg("kv")
-    ms_attn_launch = sum(hev.ms(a) for e in attn_evs for a in e) / (n_attn_steps * w.L)
-    hev.close()
-
+    buf = alloc_step(w, Eg, tg)
+    step = make_step(w, Eg, wg, tg, buf)
+    log(f"[bench] warmup {args.warmup}, timing {args.steps} steps")
+    m = measure_step(w, step, args.steps, args.warmup)
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    f_down = 2.0 * w.T * w.d * w.r * w.L
-    f_up = 2.0 * w.T * w.r * w.d * w.L
-    f_kv = 2.0 * w.T * 2 * w.kv * w.d * w.L
-    f_build = f_down + f_up + f_kv
-    f_attn = configs.flops_attention(w)
-    b_attn = configs.bytes_attention(w)
-    ms_build = ms_down + ms_up + ms_kv
-    ms_attn_total = ms_step - ms_build
-    kv_tflops = f_kv / (ms_kv * 1e-3) / 1e12
+    fig = step_figures(w, m, peak)
+    ms_step, kv_tflops = m["ms_step"], fig["kv_tflops"]
     out = {
         "metric": METRIC,
         "value": w.T / (ms_step * 1e-3),
@@ -325,22 +417,16 @@ def run_prefill(args, w):
         "roofline": {"bound": "mfma", "kernel": "k_kv_proj", "achieved": kv_tflops, "peak": peak,
                      "unit": "TFLOP/s", "frac": kv_tflops / peak,
                      "traffic": stored_traffic() if w.name == "llava7b" else None,
-                     "algorithmic_flops_per_launch": f_kv, "ms_per_launch": ms_kv},
-        "stages": {
-            "build_kv_visual_tokens_per_s": w.T / (ms_build * 1e-3),
-            "build_kv_ms": ms_build,
-            "build_kv_tflops": f_build / (ms_build * 1e-3) / 1e12,
-            "build_kv_mfma_frac": f_build / (ms_build * 1e-3) / 1e12 / peak,
-            "down_ms": ms_down, "up_ms": ms_up, "kv_ms": ms_kv,
-            "attention_ms_all_layers": ms_attn_total,
-            "attention_kernel_ms_per_layer": ms_attn_launch,
-            "attention_tflops": f_attn / (ms_attn_total * 1e-3) / 1e12,
-            "attention_gbs": b_attn / (ms_attn_total * 1e-3) / 1e9,
-            "attention_hbm_frac": b_attn / (ms_attn_total * 1e-3) / 1e9 / PEAK_HBM_GBS,
-            "step_mfma_frac": (f_build + f_attn) / (ms_step * 1e-3) / 1e12 / peak,
-        },
+                     "algorithmic_flops_per_launch": fig["f_kv"], "ms_per_launch": m["kv"]},
+        "stages": fig["stages"],
     }
-    out["step_ms_warm"] = percentiles(step_ms)
+    out["target"] = {
+        "what": "whole step (build + K/V + attention of every layer): algorithmic FLOPs / step "
+                "time / bf16 MFMA peak",
+        "value": fig["stages"]["step_mfma_frac"], "goal": 0.60,
+        "met": fig["stages"]["step_mfma_frac"] >= 0.60,
+        "step_ms_for_goal": (fig["f_build"] + fig["f_attn"]) / (0.60 * peak * 1e12) * 1e3}
+    out["step_ms_warm"] = percentiles(m["step_ms"])
     if w.dtype == "bf16":
         log("[bench] MFMA-rate probe")
         probe = mfma_probe()
@@ -352,14 +438,59 @@ def run_prefill(args, w):
         out["step_ms_cold"] = percentiles(time_calls(step, max(3, args.steps // 4), 1, flush))
         del flush
     if not args.no_variants:
-        out["variants"] = run_variants(args, w, Eg, wg, tg, peak, f_build, ms_step)
+        out["variants"] = run_variants(args, w, Eg, wg, tg, peak, fig["f_build"], ms_step)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle baseline")
         vc = synth.make_visual_cache(w, layers=[0])
         out["cpu_baseline"] = cpu_baseline(w, E, wts, {k: v[:1] for k, v in tx.items()}, vc)
-    del Eg, wg, tg, Z, Kv, Vv, O, ws_kv, ws_at
+    del Eg, wg, tg, buf, step
     torch.cuda.empty_cache()
     return out
+
+
+def run_workload_block(args, w):
+    """Compact figures of another prefill workload, inputs drawn on the GPU (same distributions
+    as the numpy generator, which would take minutes at these sizes)."""
+    import torch
+
+    from paper_2609_34972_amd import synth
+
+    dev = torch.device("cuda:0")
+    log(f"[bench] {w.name}: generating inputs on the GPU")
+    x = synth.make_on_device(w, dev, seed=0)
+    Eg = x.pop("E")
+    tg = {k: x.pop(k) for k in ("Q", "Kt", "Vt")}
+    wg = x
+    buf = alloc_step(w, Eg, tg)
+    step = make_step(w, Eg, wg, tg, buf)
+    steps = max(5, args.steps // 2)
+    log(f"[bench] {w.name}: timing {steps} steps")
+    m = measure_step(w, step, steps, 2)
+    peak = PEAK_BF16_TFLOPS
+    fig = step_figures(w, m, peak)
+    st = fig["stages"]
+    mfma_bound = w.Hq // w.Hkv * w.Nq > 315  # attention arithmetic intensity above the ridge
+    res = {
+        "config": {"batch": w.B, "visual_tokens": w.Nv, "text_tokens": w.Nt, "layers": w.L,
+                   "d": w.d, "rank": w.r, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.hd},
+        "data": "synthetic, drawn on the GPU",
+        "ms_per_step": m["ms_step"], "step_ms_warm": percentiles(m["step_ms"]),
+        "visual_tokens_per_s": w.T / (m["ms_step"] * 1e-3),
+        "step_mfma_frac": st["step_mfma_frac"],
+        "build_kv_ms": st["build_kv_ms"], "build_kv_mfma_frac": st["build_kv_mfma_frac"],
+        "down_ms": st["down_ms"], "up_ms": st["up_ms"],
+        "k_kv_proj": {"ms": m["kv"], "tflops": fig["kv_tflops"], "frac": fig["kv_tflops"] / peak},
+        "attention": {"kernel_ms_per_layer": m["attn_launch"],
+                      "bound": "mfma" if mfma_bound else "hbm",
+                      "frac": st["attention_kernel_mfma_frac"] if mfma_bound
+                      else st["attention_kernel_hbm_frac"],
+                      "tflops": fig["f_attn"] / w.L / (m["attn_launch"] * 1e-3) / 1e12,
+                      "gbs": st["attention_kernel_gbs"],
+                      "ms_all_layers_in_step": st["attention_ms_all_layers"]},
+    }
+    del x, Eg, tg, wg, buf, step
+    torch.cuda.empty_cache()
+    return res
 
 
 def run_variants(args, w, Eg, wg, tg, peak, f_build, ms_full_step):
@@ -624,6 +755,7 @@ def main():
                          "ms_per_launch": d["ms_per_layer"]},
             "delta_write": d,
         }
+        out["provenance"] = provenance()
         print(json.dumps(out), flush=True)
         return
     w = configs.get(args.workload)
@@ -646,6 +778,9 @@ def main():
         }
     else:
         out = run_prefill(args, w)
+        if w.name == "llava7b" and not args.no_workloads:
+            out["workloads"] = {o.name: run_workload_block(args, o)
+                                for o in (configs.LLAVA_NEXT, configs.QWEN25VL_VIDEO)}
         if not args.no_decode:
             out["decode"] = run_decode(args, configs.DECODE)
         if not args.no_delta:
@@ -659,6 +794,7 @@ def main():
         torch.cuda.synchronize()
         out["calibration_copy_bytes"] = n
         del src, dst
+    out["provenance"] = provenance()
     print(json.dumps(out), flush=True)
 
 

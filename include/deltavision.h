@@ -188,7 +188,10 @@ dv_status dv_kept_visual_kv(const void* E, const void* Dw, const void* Uw, const
  * text key q_pos0). Nv may be 0 (visual read blocked).
  *   Q, O   [B, Nq, Hq, hd]
  *   Kv, Vv [B, Hkv, Nv, hd]   one layer of the visual cache (may be NULL when Nv == 0)
- *   Kt, Vt [B, Hkv, Nkt, hd]  text key / value cache; requires q_pos0 + Nq <= Nkt
+ *   Kt, Vt [B, Hkv, Nkt, hd]  text key / value cache; requires q_pos0 + Nq <= Nkt (text keys
+ *          past q_pos0 + Nq - 1, e.g. the free slots of a preallocated cache, are never read)
+ *   Sizes: one (batch, kv-head) slice of either cache holds at most 2^31-1 bytes
+ *          (Nv*hd*elem_size and Nkt*hd*elem_size), otherwise DV_ERR_SHAPE
  *   scale  softmax scale, finite and > 0, usually 1/sqrt(hd)
  *   ws     split-key partials; may be NULL/0 (then keys are not split). With
  *          dv_text_visual_attention_workspace(...) bytes the call picks its

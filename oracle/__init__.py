@@ -60,8 +60,6 @@ def _load():
         lib.dvref_kv_epilogue.restype = i32
         lib.dvref_delta_rule.argtypes = [P, P, P, P, P] + [i32] * 6
         lib.dvref_delta_rule.restype = i32
-        lib.dvref_attention_weights.argtypes = [P, P, P, P] + [i32] * 8 + [f64, i32, i32, i32]
-        lib.dvref_attention_weights.restype = i32
         _lib = lib
         return lib
 
@@ -153,23 +151,6 @@ def text_visual_attention(Q: np.ndarray, Kv: np.ndarray, Vv: np.ndarray, Kt: np.
     if rc != 0:
         raise ValueError("invalid attention shape")
     return O
-
-
-def attention_weights(Q, Kv, Kt, q_pos0: int, b: int, i: int, h: int,
-                      scale: Optional[float] = None) -> np.ndarray:
-    """Softmax weights of query (b, i, h) over its key set (visual first, then text)."""
-    Q, Kv, Kt = map(_c, (Q, Kv, Kt))
-    B, Nq, Hq, hd = Q.shape
-    _, Hkv, Nv, _ = Kv.shape
-    Nkt = Kt.shape[2]
-    if scale is None:
-        scale = hd ** -0.5
-    p = np.empty(Nv + Nkt)
-    n = _load().dvref_attention_weights(_p(Q), _p(Kv), _p(Kt), _p(p), B, Hq, Hkv, hd, Nv, Nq,
-                                        Nkt, int(q_pos0), float(scale), b, i, h)
-    if n < 0:
-        raise ValueError("invalid attention shape")
-    return p[:n].copy()
 
 
 def kv_epilogue(Kv, Vv, k_bias=None, v_bias=None, k_norm=None, kn_eps: float = 1e-6, pos=None,

@@ -294,31 +294,3 @@ int dvref_text_visual_attention(const double* Q, const double* Kv, const double*
   }
   return 0;
 }
-
-/* Softmax weights of one query row of Eq. 9, exposed so tests can check that they are a
- * probability distribution. Writes Nv + q_pos0 + i + 1 weights into p. */
-int dvref_attention_weights(const double* Q, const double* Kv, const double* Kt, double* p, int B,
-                            int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt, int q_pos0,
-                            double scale, int b, int i, int h) {
-  if (q_pos0 < 0 || q_pos0 + Nq > Nkt || Hq % Hkv != 0) return -1;
-  const int g = h / (Hq / Hkv);
-  const double* q = Q + (((int64_t)b * Nq + i) * Hq + h) * hd;
-  const double* kv = Kv + ((int64_t)b * Hkv + g) * (int64_t)Nv * hd;
-  const double* kt = Kt + ((int64_t)b * Hkv + g) * (int64_t)Nkt * hd;
-  const int n = Nv + q_pos0 + i + 1;
-  double mx = -INFINITY;
-  for (int j = 0; j < n; ++j) {
-    const double* key = (j < Nv) ? kv + (int64_t)j * hd : kt + (int64_t)(j - Nv) * hd;
-    double dot = 0.0;
-    for (int c = 0; c < hd; ++c) dot += q[c] * key[c];
-    p[j] = scale * dot;
-    mx = p[j] > mx ? p[j] : mx;
-  }
-  double denom = 0.0;
-  for (int j = 0; j < n; ++j) {
-    p[j] = exp(p[j] - mx);
-    denom += p[j];
-  }
-  for (int j = 0; j < n; ++j) p[j] /= denom;
-  return n;
-}

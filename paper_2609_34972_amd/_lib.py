@@ -165,6 +165,16 @@ def _stream(device: torch.device, stream=None) -> int:
     return s.cuda_stream
 
 
+def _workspace(nbytes: int, device: torch.device, stream=None) -> torch.Tensor:
+    """A temporary workspace for one call. The caching allocator ties a block to the stream it
+    was allocated on; when the work runs on another stream, record that stream so the block is
+    not handed out again before the enqueued kernels are done with it."""
+    ws = torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+    if stream is not None:
+        ws.record_stream(stream)
+    return ws
+
+
 def time_kernel(kernel: int, begin: Optional[int] = None, end: Optional[int] = None) -> None:
     """Bracket every later launch of `kernel` on this thread with two hipEvent_t handles
     (raw integers, e.g. from hipEventCreate); time_kernel(kernel) switches the hook off."""
@@ -243,8 +253,7 @@ def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, l0: int = 0,
     lib = load()
     if epilogue is None:
         if ws is None:
-            ws = torch.empty(project_visual_kv_workspace(T, d, nl, E.dtype), dtype=torch.uint8,
-                             device=E.device)
+            ws = _workspace(project_visual_kv_workspace(T, d, nl, E.dtype), E.device, stream)
         _check(lib.dv_project_visual_kv(_ptr(E), _ptr(Z), _ptr(Uw), _ptr(gamma), _ptr(Wk),
                                         _ptr(Wv), _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, l0,
                                         nl, float(eps), code, _ptr(ws), ws.numel(),
@@ -252,8 +261,7 @@ def project_visual_kv(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, l0: int = 0,
         return Kv, Vv
     st = _epilogue_struct(epilogue, L, B, Nv, Hkv, hd, E.dtype)
     if ws is None:
-        ws = torch.empty(project_visual_kv_ex_workspace(T, d, nl, hd, E.dtype), dtype=torch.uint8,
-                         device=E.device)
+        ws = _workspace(project_visual_kv_ex_workspace(T, d, nl, hd, E.dtype), E.device, stream)
     _check(lib.dv_project_visual_kv_ex(_ptr(E), _ptr(Z), _ptr(Uw), _ptr(gamma), _ptr(Wk), _ptr(Wv),
                                        _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, l0, nl,
                                        float(eps), ctypes.byref(st), code, _ptr(ws), ws.numel(),
@@ -278,8 +286,7 @@ def recurrent_visual_kv(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv, eps: float, act: int =
         raise ValueError("shape mismatch in recurrent_visual_kv")
     code = _dtype_code(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv)
     if ws is None:
-        ws = torch.empty(recurrent_visual_kv_workspace(T, d, L, r, E.dtype), dtype=torch.uint8,
-                         device=E.device)
+        ws = _workspace(recurrent_visual_kv_workspace(T, d, L, r, E.dtype), E.device, stream)
     _check(load().dv_recurrent_visual_kv(_ptr(E), _ptr(Dw), _ptr(Uw), _ptr(gamma), _ptr(Wk),
                                          _ptr(Wv), _ptr(Kv), _ptr(Vv), B, Nv, d, L, r, Hkv, hd, act,
                                          float(eps), code, _ptr(ws), ws.numel(),
@@ -313,8 +320,7 @@ def kept_visual_kv(E, Dw, Uw, gamma, Wk, Wv, keep, Kv, Vv, eps: float, act: int 
         raise ValueError("shape mismatch in kept_visual_kv")
     code = _dtype_code(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv)
     if ws is None:
-        ws = torch.empty(kept_visual_kv_workspace(T, d, r, nkeep, E.dtype), dtype=torch.uint8,
-                         device=E.device)
+        ws = _workspace(kept_visual_kv_workspace(T, d, r, nkeep, E.dtype), E.device, stream)
     keep_arr = (ctypes.c_uint8 * L).from_buffer_copy(flags)
     _check(load().dv_kept_visual_kv(_ptr(E), _ptr(Dw), _ptr(Uw), _ptr(gamma), _ptr(Wk), _ptr(Wv),
                                     ctypes.cast(keep_arr, ctypes.c_void_p), _ptr(Kv), _ptr(Vv), B,
@@ -343,8 +349,7 @@ def delta_rule_write(k, v, alpha, beta, S, ws: Optional[torch.Tensor] = None, st
             raise ValueError("alpha, beta and S must be contiguous device tensors")
     code = _dtype_code(k, v)
     if ws is None:
-        n = delta_rule_workspace(B, Hv, N, dk, dv, k.dtype)
-        ws = torch.empty(max(n, 16), dtype=torch.uint8, device=k.device)
+        ws = _workspace(delta_rule_workspace(B, Hv, N, dk, dv, k.dtype), k.device, stream)
     _check(load().dv_delta_rule_write(_ptr(k), _ptr(v), alpha.data_ptr(), beta.data_ptr(),
                                       S.data_ptr(), B, Hk, Hv, N, dk, dv, code, _ptr(ws),
                                       ws.numel(), _stream(k.device, stream)))
@@ -374,7 +379,7 @@ def text_visual_attention(Q, Kv, Vv, Kt, Vt, O, q_pos0: int = 0, scale: Optional
         scale = hd ** -0.5
     if ws is None:
         n = text_visual_attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nkt)
-        ws = torch.empty(max(n, 16), dtype=torch.uint8, device=Q.device) if n else None
+        ws = _workspace(n, Q.device, stream) if n else None
     kvp = _ptr(Kv) if Nv > 0 else None
     vvp = _ptr(Vv) if Nv > 0 else None
     _check(load().dv_text_visual_attention(_ptr(Q), kvp, vvp, _ptr(Kt), _ptr(Vt), _ptr(O), B, Hq,
@@ -383,3 +388,4 @@ def text_visual_attention(Q, Kv, Vv, Kt, Vt, O, q_pos0: int = 0, scale: Optional
                                            ws.numel() if ws is not None else 0,
                                            _stream(Q.device, stream)))
     return O
+

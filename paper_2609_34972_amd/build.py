@@ -5,6 +5,8 @@ Packed-fp32 VALU instructions are disabled for every device compilation.
 """
 from __future__ import annotations
 
+import hashlib
+import json
 import os
 import subprocess
 import sys
@@ -14,6 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdeltavision.so")
+INFO = os.path.join(HERE, "build_info.json")
 SOURCES = ["api.cpp", "build_kernels.hip", "attention.hip", "recurrent.hip", "delta_rule.hip",
            "probe.hip"]
 ARCH = "gfx950"
@@ -43,6 +46,34 @@ def _compile(src: str) -> str:
     return out
 
 
+def sources_digest() -> str:
+    """Short sha256 over the library's sources (and this build script)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)) + [os.path.join("..", "build.py")]:
+        path = os.path.join(CSRC, name)
+        if os.path.isfile(path):
+            with open(path, "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def _write_build_info() -> None:
+    """Record which sources the library was built from (read by the benchmark, which runs where
+    no git metadata is available)."""
+    def git(*a):
+        try:
+            r = subprocess.run(["git", *a], cwd=HERE, capture_output=True, text=True, timeout=10)
+            return r.stdout.strip() if r.returncode == 0 else None
+        except (OSError, subprocess.SubprocessError):
+            return None
+    info = {"git_rev": git("rev-parse", "HEAD"),
+            "git_dirty": bool(git("status", "--porcelain", "--", "."))
+            if git("rev-parse", "HEAD") else None,
+            "sources_sha256_16": sources_digest(), "arch": ARCH}
+    with open(INFO, "w") as f:
+        json.dump(info, f)
+
+
 def build() -> str:
     """Compile every HIP source for gfx950 and link the shared library. Returns its path."""
     os.makedirs(BUILD, exist_ok=True)
@@ -52,6 +83,7 @@ def build() -> str:
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    _write_build_info()
     return LIB
 
 

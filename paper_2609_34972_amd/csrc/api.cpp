@@ -447,11 +447,15 @@ size_t dv_text_visual_attention_workspace(int32_t B, int32_t Hq, int32_t Hkv, in
   return dv::attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nkt);
 }
 
-dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv, const void* Kt,
-                                   const void* Vt, void* O, int32_t B, int32_t Hq, int32_t Hkv,
-                                   int32_t hd, int32_t Nv, int32_t Nq, int32_t Nkt,
-                                   int32_t q_pos0, float scale, int32_t dtype, void* ws,
-                                   size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation shared by both attention entry points; nothing is enqueued here.
+dv_status check_attention(const void* Q, const void* Kv, const void* Vv, const void* Kt,
+                          const void* Vt, const void* O, int32_t B, int32_t Hq, int32_t Hkv,
+                          int32_t hd, int32_t Nv, int32_t Nq, int32_t Nkt, int32_t q_pos0,
+                          float scale, int32_t dtype) {
   DV_CHECK(check_dtype(dtype));
   if (B <= 0 || Hq <= 0 || Hkv <= 0 || hd <= 0 || Nv < 0 || Nq <= 0 || Nkt <= 0 || q_pos0 < 0)
     return fail(DV_ERR_SHAPE,
@@ -465,6 +469,12 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
     return fail(DV_ERR_SHAPE, "key count exceeds 2^30 or B*Nq*Hq exceeds 2^23");
   if ((int64_t)B * Hkv > 65535) return fail(DV_ERR_SHAPE, "B*Hkv=%lld exceeds 65535", (long long)B * Hkv);
   if (hd != 64 && hd != 128) return fail(DV_ERR_UNSUPPORTED, "hd=%d must be 64 or 128", hd);
+  // The streaming kernels address one (batch, kv-head) slice of a cache through a buffer
+  // resource with a 32-bit byte range and 32-bit offsets.
+  if ((int64_t)Nv * hd * (int64_t)elem_size(dtype) > INT32_MAX ||
+      (int64_t)Nkt * hd * (int64_t)elem_size(dtype) > INT32_MAX)
+    return fail(DV_ERR_SHAPE, "a (batch, kv-head) cache slice exceeds 2^31-1 bytes (Nv=%d Nkt=%d hd=%d)",
+                Nv, Nkt, hd);
   if (!std::isfinite(scale) || !(scale > 0.f))
     return fail(DV_ERR_SHAPE, "scale must be finite and > 0");
   DV_CHECK(need_ptr(Q, "Q"));
@@ -475,10 +485,14 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
   DV_CHECK(need_ptr(Kt, "Kt"));
   DV_CHECK(need_ptr(Vt, "Vt"));
   DV_CHECK(need_ptr(O, "O"));
-  if (ws && !aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
-  const dv::AttnPlan plan =
-      dv::plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, dtype == DV_BF16 ? 1 : 0,
-                         ws ? ws_bytes : 0);
+  return DV_OK;
+}
+
+dv_status run_attention(const void* Q, const void* Kv, const void* Vv, const void* Kt,
+                        const void* Vt, void* O, int32_t B, int32_t Hq, int32_t Hkv, int32_t hd,
+                        int32_t Nv, int32_t Nq, int32_t Nkt, int32_t q_pos0, float scale,
+                        int32_t dtype, void* ws, const dv::AttnPlan& plan, hipStream_t stream,
+                        const char* name) {
   dv::AttnArgs a{};
   a.Q = Q;
   a.Kv = Kv;
@@ -501,9 +515,26 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
   a.splits = plan.splits;
   a.keys_per_split = plan.keys_per_split;
   a.tiles_per_split = plan.tiles_per_split;
-  return hip_status(dv::launch_attention(a, plan, dtype == DV_BF16 ? 1 : 0, (hipStream_t)stream,
-                                         g_ev),
-                    "dv_text_visual_attention launch");
+  return hip_status(dv::launch_attention(a, plan, dtype == DV_BF16 ? 1 : 0, stream, g_ev), name);
+}
+
+}  // namespace
+
+extern "C" {
+
+dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv, const void* Kt,
+                                   const void* Vt, void* O, int32_t B, int32_t Hq, int32_t Hkv,
+                                   int32_t hd, int32_t Nv, int32_t Nq, int32_t Nkt,
+                                   int32_t q_pos0, float scale, int32_t dtype, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  DV_CHECK(check_attention(Q, Kv, Vv, Kt, Vt, O, B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, scale,
+                           dtype));
+  if (ws && !aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
+  const dv::AttnPlan plan =
+      dv::plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, dtype == DV_BF16 ? 1 : 0,
+                         ws ? ws_bytes : 0);
+  return run_attention(Q, Kv, Vv, Kt, Vt, O, B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, scale, dtype,
+                       ws, plan, (hipStream_t)stream, "dv_text_visual_attention launch");
 }
 
 }  // extern "C"

@@ -1090,13 +1090,18 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
       return hipErrorInvalidValue;  // the planner only picks this kernel for bf16, hd 128
     }
   } else {
-    dim3 grid(p.row_blocks, a.B * a.Hkv, p.splits);
-    if (p.nw == 1)
-      k_attn_prefill<T, HD, 1><<<grid, dim3(64), AttnCfg<T, HD, 1>::LDS_BYTES, s>>>(a);
-    else if (p.nw == 2)
-      k_attn_prefill<T, HD, 2><<<grid, dim3(128), AttnCfg<T, HD, 2>::LDS_BYTES, s>>>(a);
-    else
-      k_attn_prefill<T, HD, 4><<<grid, dim3(256), AttnCfg<T, HD, 4>::LDS_BYTES, s>>>(a);
+    // bf16 hd-128 prefill always takes the streaming kernels, so no such instance is built.
+    if constexpr (sizeof(T) == 2 && HD == 128) {
+      return hipErrorInvalidValue;
+    } else {
+      dim3 grid(p.row_blocks, a.B * a.Hkv, p.splits);
+      if (p.nw == 1)
+        k_attn_prefill<T, HD, 1><<<grid, dim3(64), AttnCfg<T, HD, 1>::LDS_BYTES, s>>>(a);
+      else if (p.nw == 2)
+        k_attn_prefill<T, HD, 2><<<grid, dim3(128), AttnCfg<T, HD, 2>::LDS_BYTES, s>>>(a);
+      else
+        k_attn_prefill<T, HD, 4><<<grid, dim3(256), AttnCfg<T, HD, 4>::LDS_BYTES, s>>>(a);
+    }
   }
   record(ev.attn[1], s);
   hipError_t e = hipGetLastError();

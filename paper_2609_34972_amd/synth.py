@@ -164,3 +164,39 @@ def make_delta_inputs(w, seed: int = 0) -> Dict[str, torch.Tensor]:
 def as_f64(t: torch.Tensor) -> np.ndarray:
     """The exact values a tensor holds, widened to fp64 for the oracle."""
     return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+def make_on_device(w: Workload, device, seed: int = 0) -> Dict[str, torch.Tensor]:
+    """E, the build weights and the text tensors of every layer drawn on the GPU, with the same
+    distributions as make_E / make_build_weights / make_text (torch's device generator instead
+    of numpy's, so the values differ). Used where the numpy draw of a large workload would take
+    minutes; operand statistics matter for timing because the chip's clock depends on them."""
+    dt = torch_dtype(w)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+
+    def normal_(shape, std=1.0, shift=0.0):
+        a = torch.randn(*shape, generator=gen, device=device, dtype=torch.float32)
+        if std != 1.0:
+            a.mul_(std)
+        if shift != 0.0:
+            a.add_(shift)
+        return a.to(dt)
+
+    def stack(shape, std=1.0, shift=0.0, L=None):
+        return torch.stack([normal_(shape, std, shift) for _ in range(w.L if L is None else L)], 0)
+
+    E = torch.randn(w.T, w.d, generator=gen, device=device, dtype=torch.float32)
+    if w.outlier_channels:
+        E[:, list(w.outlier_channels)] *= w.outlier_scale
+    return {
+        "E": E.to(dt),
+        "Dw": stack((w.r, w.d), w.d ** -0.5),
+        "Uw": stack((w.d, w.r), w.r ** -0.5),
+        "gamma": stack((w.d,), 0.1, 1.0),
+        "Wk": stack((w.kv, w.d), w.d ** -0.5),
+        "Wv": stack((w.kv, w.d), w.d ** -0.5),
+        "Q": stack((w.B, w.Nq, w.Hq, w.hd)),
+        "Kt": stack((w.B, w.Hkv, w.Nkt, w.hd)),
+        "Vt": stack((w.B, w.Hkv, w.Nkt, w.hd)),
+    }

@@ -182,6 +182,8 @@ def sdpa_reference(Q, Kv, Vv, Kt, Vt, q_pos0):
     (2, 4, 4, 16, 9, 5, 5, 0),      # MHA prefill
     (1, 6, 2, 8, 13, 4, 7, 3),      # GQA, queries start after 3 text tokens
     (3, 2, 1, 32, 1, 1, 6, 5),      # decode-like single query at position 5
+    (2, 4, 2, 16, 9, 3, 12, 4),     # text cache longer than the queries' positions (keys 7..11 unused)
+    (1, 2, 2, 16, 5, 1, 10, 4),     # decode into a preallocated cache of 10 text slots
 ])
 def test_attention_matches_sdpa(B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0):
     Q = rnd(40, B, Nq, Hq, hd)
@@ -201,14 +203,28 @@ def test_attention_without_visual_keys_is_causal_attention():
     np.testing.assert_allclose(O, ref.transpose(1, 2).numpy(), rtol=1e-12, atol=1e-13)
 
 
-def test_attention_weights_are_distributions():
-    B, Hq, Hkv, hd, Nv, Nq, Nkt = 1, 2, 1, 16, 11, 4, 4
-    Q, Kv, Kt = rnd(48, B, Nq, Hq, hd, scale=3.0), rnd(49, B, Hkv, Nv, hd), rnd(50, B, Hkv, Nkt, hd)
-    for i in range(Nq):
-        p = oracle.attention_weights(Q, Kv, Kt, 0, 0, i, 1)
-        assert p.shape == (Nv + i + 1,)
-        assert abs(p.sum() - 1.0) < 1e-14
-        assert np.all(p > 0)
+def test_attention_weights_match_softmax_and_are_distributions():
+    """With one-hot value rows (value j = unit vector e_j) the output of Eq. 9 is the weight
+    vector itself, so the oracle's weights can be read off and compared with torch's softmax of
+    scale * Q K^T under the Eq. 9 mask: this pins the score scale, the mask (including text keys
+    past the queries' positions in a longer cache) and the normalisation of the real function."""
+    B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0 = 2, 4, 2, 24, 9, 4, 11, 3
+    Q = rnd(48, B, Nq, Hq, hd, scale=3.0)
+    Kv, Kt = rnd(49, B, Hkv, Nv, hd), rnd(50, B, Hkv, Nkt, hd)
+    eye = np.eye(hd)
+    Vv = np.broadcast_to(eye[:Nv], (B, Hkv, Nv, hd)).copy()
+    Vt = np.broadcast_to(eye[Nv:Nv + Nkt], (B, Hkv, Nkt, hd)).copy()
+    for scale in (None, 0.3):
+        P = oracle.text_visual_attention(Q, Kv, Vv, Kt, Vt, q_pos0, scale=scale)[..., :Nv + Nkt]
+        s = hd ** -0.5 if scale is None else scale
+        K = torch.cat([t64(Kv), t64(Kt)], dim=2).repeat_interleave(Hq // Hkv, dim=1)
+        scores = s * torch.matmul(t64(Q).transpose(1, 2), K.transpose(2, 3))  # [B, Hq, Nq, keys]
+        mask = torch.from_numpy(key_mask(Nv, Nq, Nkt, q_pos0))
+        ref = torch.softmax(scores.masked_fill(~mask, float("-inf")), dim=-1).transpose(1, 2)
+        np.testing.assert_allclose(P, ref.numpy(), rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(P.sum(axis=-1), 1.0, rtol=0, atol=1e-14)
+        allowed = np.broadcast_to(key_mask(Nv, Nq, Nkt, q_pos0)[None, :, None, :], P.shape)
+        assert np.all(P[allowed] > 0) and np.all(P[~allowed] == 0)
 
 
 def test_attention_closed_forms():
