@@ -206,6 +206,27 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
                                    size_t ws_bytes, void* stream);
 
 /*
+ * dv_text_visual_attention for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc). Same arguments, same result
+ * bits as dv_text_visual_attention with its recommended workspace, but the key-split partials
+ * live in a static array of DV_ATTENTION_SCRATCH_BYTES inside the library: each GPU the library
+ * runs on holds its own copy until the process ends. The call allocates and frees nothing and
+ * clears nothing (every partial is written before it is read). A call whose key split needs
+ * more partials than the array holds returns DV_ERR_WORKSPACE without launching (the
+ * LLaVA-NeXT-sized prefill, 8 x 128 queries x 32 heads over 2880 visual keys, is one); such
+ * calls go through dv_text_visual_attention with a workspace.
+ * All calls on one GPU share its array: calls that may overlap on one GPU (different streams,
+ * or different threads without ordering) race on it and must be serialised by the caller.
+ * The stream must belong to the current device.
+ */
+#define DV_ATTENTION_SCRATCH_BYTES ((size_t)32 << 20)
+dv_status dv_text_visual_attention_noalloc(const void* Q, const void* Kv, const void* Vv,
+                                           const void* Kt, const void* Vt, void* O, int32_t B,
+                                           int32_t Hq, int32_t Hkv, int32_t hd, int32_t Nv,
+                                           int32_t Nq, int32_t Nkt, int32_t q_pos0, float scale,
+                                           int32_t dtype, void* stream);
+
+/*
  * Visual write into a linear-attention (Gated DeltaNet) recurrent state (appendix on linear
  * attention, Eq. 15-16): for every sequence b and value head h, the visual tokens t = 0..N-1
  * are written in order,

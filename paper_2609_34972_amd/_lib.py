@@ -28,6 +28,7 @@ EXPORTS = (
     "dv_project_visual_kv",
     "dv_text_visual_attention_workspace",
     "dv_text_visual_attention",
+    "dv_text_visual_attention_noalloc",
     "dv_status_string",
     "dv_last_error",
     "dv_abi_version",
@@ -109,6 +110,8 @@ def load() -> ctypes.CDLL:
         lib.dv_text_visual_attention_workspace.restype = sz
         lib.dv_text_visual_attention.argtypes = [vp] * 6 + [i32] * 8 + [f32, i32, vp, sz, vp]
         lib.dv_text_visual_attention.restype = i32
+        lib.dv_text_visual_attention_noalloc.argtypes = [vp] * 6 + [i32] * 8 + [f32, i32, vp]
+        lib.dv_text_visual_attention_noalloc.restype = i32
         lib.dv_status_string.argtypes = [i32]
         lib.dv_status_string.restype = ctypes.c_char_p
         lib.dv_last_error.argtypes = []
@@ -389,3 +392,32 @@ def text_visual_attention(Q, Kv, Vv, Kt, Vt, O, q_pos0: int = 0, scale: Optional
                                            _stream(Q.device, stream)))
     return O
 
+
+ATTENTION_SCRATCH_BYTES = 32 << 20  # DV_ATTENTION_SCRATCH_BYTES
+
+
+def text_visual_attention_noalloc(Q, Kv, Vv, Kt, Vt, O, q_pos0: int = 0,
+                                  scale: Optional[float] = None, stream=None):
+    """text_visual_attention without a workspace: the key-split partials live in the library's
+    static per-GPU scratch, so the call allocates nothing. Calls that may overlap on one GPU
+    share that scratch and must be serialised by the caller."""
+    B, Nq, Hq, hd = Q.shape
+    _, Hkv, Nkt, _ = Kt.shape
+    if Kv is None or Vv is None:
+        if Kv is not None or Vv is not None:
+            raise ValueError("Kv and Vv must both be given or both be None")
+        Nv = 0
+    else:
+        Nv = Kv.shape[2]
+        if tuple(Kv.shape) != (B, Hkv, Nv, hd) or Vv.shape != Kv.shape:
+            raise ValueError("shape mismatch in text_visual_attention_noalloc")
+    if (Vt.shape != Kt.shape or Kt.shape[0] != B or Kt.shape[3] != hd or O.shape != Q.shape):
+        raise ValueError("shape mismatch in text_visual_attention_noalloc")
+    code = _dtype_code(*[t for t in (Q, Kv, Vv, Kt, Vt, O) if t is not None])
+    if scale is None:
+        scale = hd ** -0.5
+    _check(load().dv_text_visual_attention_noalloc(
+        _ptr(Q), _ptr(Kv) if Nv > 0 else None, _ptr(Vv) if Nv > 0 else None, _ptr(Kt), _ptr(Vt),
+        _ptr(O), B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, float(scale), code,
+        _stream(Q.device, stream)))
+    return O

@@ -537,4 +537,28 @@ dv_status dv_text_visual_attention(const void* Q, const void* Kv, const void* Vv
                        ws, plan, (hipStream_t)stream, "dv_text_visual_attention launch");
 }
 
+dv_status dv_text_visual_attention_noalloc(const void* Q, const void* Kv, const void* Vv,
+                                           const void* Kt, const void* Vt, void* O, int32_t B,
+                                           int32_t Hq, int32_t Hkv, int32_t hd, int32_t Nv,
+                                           int32_t Nq, int32_t Nkt, int32_t q_pos0, float scale,
+                                           int32_t dtype, void* stream) {
+  DV_CHECK(check_attention(Q, Kv, Vv, Kt, Vt, O, B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, scale,
+                           dtype));
+  // The split dv_text_visual_attention takes with its recommended workspace, so both entry
+  // points give the same bits; a split whose partials exceed the static scratch is refused.
+  const dv::AttnPlan plan = dv::plan_attention(B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0,
+                                               dtype == DV_BF16 ? 1 : 0, (size_t)-1);
+  const size_t cap = dv::attention_scratch_bytes();
+  if (plan.ws_needed > cap)
+    return fail(DV_ERR_WORKSPACE,
+                "this call's key split needs %zu bytes of partials, more than the %zu bytes of the "
+                "static scratch; call dv_text_visual_attention with a workspace instead",
+                plan.ws_needed, cap);
+  void* scr = nullptr;  // resolved on the first call on each device
+  hipError_t e = dv::attention_scratch(&scr);
+  if (e != hipSuccess) return hip_status(e, "dv_text_visual_attention_noalloc scratch lookup");
+  return run_attention(Q, Kv, Vv, Kt, Vt, O, B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0, scale, dtype,
+                       plan.splits > 1 ? scr : nullptr, plan, (hipStream_t)stream, "dv_text_visual_attention_noalloc launch");
+}
+
 }  // extern "C"

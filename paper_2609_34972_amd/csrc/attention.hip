@@ -25,6 +25,10 @@
 
 #include <math.h>
 
+#include <mutex>
+
+#include "../../include/deltavision.h"
+
 namespace dv {
 
 constexpr float NEG_BIG = -1e30f;  // finite start value of the running max
@@ -1110,6 +1114,40 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
   const int64_t threads = rows * (HD / 4);
   k_attn_combine<T, HD><<<dim3((unsigned)cdiv64(threads, 256)), dim3(256), 0, s>>>((const float*)a.Opart, (const float*)a.MLpart, (T*)a.O, rows, p.splits);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ static scratch
+//
+// Key-split partials of dv_text_visual_attention_noalloc, for callers that cannot allocate. Each
+// GPU holds its own copy of this array for the life of the process. In host code `scratch` names
+// a host-side stand-in, not device memory: kernels get the device address that
+// hipGetSymbolAddress returns for the current device, looked up once per device.
+
+static __device__ __align__(256) unsigned char scratch[DV_ATTENTION_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+size_t attention_scratch_bytes() { return DV_ATTENTION_SCRATCH_BYTES; }
+
+hipError_t attention_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int dtype, hipStream_t s,

@@ -43,5 +43,9 @@ AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt,
 size_t attention_workspace(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt);
 hipError_t launch_attention(const AttnArgs& a, const AttnPlan& p, int dtype, hipStream_t s,
                             const LaunchEvents& ev);
+// Address of the library's static scratch array (attention_scratch_bytes() bytes) on the
+// current device; resolved once per device.
+hipError_t attention_scratch(void** ptr);
+size_t attention_scratch_bytes();
 
 }  // namespace dv

@@ -296,3 +296,22 @@ def test_delta_rule_workspace_scales_with_chunks(lib):
 def test_probe_mfma_rejects(lib, sink, iters, code):
     assert lib.dv_probe_mfma(1, iters, sink, None) == code
     assert lib.dv_last_error() != b""
+
+
+def noalloc_call(lib, Q=FAKE, Kv=FAKE, Vv=FAKE, Kt=FAKE, Vt=FAKE, O=FAKE, B=2, Hq=8, Hkv=2, hd=64,
+                 Nv=300, Nq=9, Nkt=20, q0=11, scale=0.125, dt=BF16):
+    return lib.dv_text_visual_attention_noalloc(Q, Kv, Vv, Kt, Vt, O, B, Hq, Hkv, hd, Nv, Nq, Nkt,
+                                                q0, scale, dt, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Q=None), NULL), (dict(O=None), NULL), (dict(Kv=None), NULL), (dict(O=FAKE + 2), ALIGN),
+    (dict(Hq=7), SHAPE), (dict(q0=12), SHAPE), (dict(scale=0.0), SHAPE), (dict(hd=96), UNSUP),
+    (dict(dt=3), UNSUP),
+    # LLaVA-NeXT-sized prefill: its preferred key split needs more partials than the static
+    # scratch holds, so the call is refused on the host
+    (dict(B=8, Hq=32, Hkv=32, hd=128, Nv=2880, Nq=128, Nkt=128, q0=0), WS),
+])
+def test_noalloc_attention_rejects(lib, kw, code):
+    assert noalloc_call(lib, **kw) == code
+    assert lib.dv_last_error() != b""
