@@ -489,20 +489,31 @@ __global__ __launch_bounds__(KvP::NT) void k_kv_proj_p(const bf16* __restrict__ 
     B = BufOperand{buffer_rsrc(Wvl + (int64_t)(n0 - kv) * d, (int64_t)(N - n0) * ldb),
                    buffer_rsrc(Wvl, 0), 1 << 30, ldb};
   }
-  // RMSNorm row scales of this block's rows, finished from the partial sums while the first
-  // operand tiles load; kept in the LDS bytes above the two pipeline stages.
+  // RMSNorm row scales of this block's rows from the partial sums of squares, two threads per
+  // row. The first 64 partials of each row are requested before the operand tiles (so their
+  // latency hides behind the pipeline's first wait) and summed, in a fixed order, after the
+  // main loop; the scales go to the LDS bytes above the two pipeline stages.
   float* rs_lds = (float*)(smem + kKvRsOffset);
-  {
-    const int rr = threadIdx.x >> 1, half = threadIdx.x & 1;  // two threads per row
-    const int row = m0 + rr;
-    float sum = 0.f;
-    if (row < T)
-      for (int p = half; p < np; p += 2) sum += ssq[((int64_t)lz * np + p) * T + row];
-    sum += __shfl_xor(sum, 1, WAVE);
-    if (half == 0) rs_lds[rr] = rsqrtf(sum / (float)d + eps);
+  const int rs_r = threadIdx.x >> 1, rs_half = threadIdx.x & 1;
+  const int rs_row = m0 + rs_r;
+  const float* rs_src = ssq + (int64_t)lz * np * T + rs_row;
+  float part[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const int p = rs_half + 2 * i;
+    part[i] = (rs_row < T && p < np) ? rs_src[(int64_t)p * T] : 0.f;
   }
   f32x4 acc[C::FM][C::FN];
-  pipe_mainloop<C>(A, B, d, (bf16*)smem, acc);  // its barriers also publish rs_lds
+  pipe_mainloop<C>(A, B, d, (bf16*)smem, acc);
+  {
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) sum += part[i];
+    if (rs_row < T)
+      for (int p = 64 + rs_half; p < np; p += 2) sum += rs_src[(int64_t)p * T];
+    sum += __shfl_xor(sum, 1, WAVE);
+    if (rs_half == 0) rs_lds[rs_r] = rsqrtf(sum / (float)d + eps);
+  }
 
   // Epilogue through LDS: every wave writes its scaled 64 x 128 tile as bf16 rows (pitch padded
   // by 16 B so the 16 rows written together hit distinct banks), then stores whole 16-byte
