@@ -24,6 +24,10 @@
  *  - Errors: arguments are validated on the host before anything is enqueued;
  *    on error nothing is launched and no output is written. A failed launch
  *    returns DV_ERR_HIP. No C++ exception crosses this boundary.
+ *  - Debugging: with DV_DEBUG set (to anything but "0") in the environment, every
+ *    call waits for the kernels it enqueued and returns DV_ERR_HIP if one of them
+ *    failed (e.g. a memory fault), so the failing call is the one that reports it.
+ *    It synchronises the stream, so it is not for streams under graph capture.
  *  - Supported: dtype f32 or bf16; hd in {64, 128}; Hq % Hkv == 0;
  *    d % 64 == 0; r % 16 == 0; all sizes > 0 unless stated.
  */

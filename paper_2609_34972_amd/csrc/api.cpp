@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 
 #include "attention.hpp"
@@ -64,6 +65,27 @@ dv_status hip_status(hipError_t e, const char* what) {
   return ok();
 }
 
+// DV_DEBUG set (and not "0") in the environment: every call waits for the kernels it enqueued and
+// reports a failure of any of them (a memory fault, an invalid launch) as DV_ERR_HIP from that
+// call, instead of from some later HIP call.
+bool debug_sync() {
+  const char* v = std::getenv("DV_DEBUG");
+  return v && *v && std::strcmp(v, "0") != 0;
+}
+
+// Status of a call whose kernels have been enqueued on stream s (launch result e).
+dv_status launched(hipError_t e, const char* what, hipStream_t s) {
+  if (e != hipSuccess) return fail(DV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  if (debug_sync()) {
+    e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = hipGetLastError();
+    if (e != hipSuccess)
+      return fail(DV_ERR_HIP, "%s: the enqueued kernels failed (DV_DEBUG): %s", what,
+                  hipGetErrorString(e));
+  }
+  return ok();
+}
+
 // Bytes of one layer's slot in the projection workspace: the gamma-weighted
 // memory in the call dtype, then the fp32 partial sums of squares.
 size_t kv_ws_layer_bytes(int64_t T, int32_t d, int32_t dtype) {
@@ -117,9 +139,8 @@ dv_status dv_probe_mfma(int32_t random, int32_t iters, float* sink, void* stream
   DV_CHECK(need_ptr(sink, "sink"));
   if (iters < 1 || iters > (1 << 20))
     return fail(DV_ERR_SHAPE, "iters=%d must lie in [1, 2^20]", iters);
-  if (dv::launch_probe_mfma(random != 0, iters, sink, (hipStream_t)stream) != hipSuccess)
-    return fail(DV_ERR_HIP, "probe launch failed");
-  return ok();
+  return launched(dv::launch_probe_mfma(random != 0, iters, sink, (hipStream_t)stream),
+                  "dv_probe_mfma launch", (hipStream_t)stream);
 }
 
 dv_status dv_build_visual_memory(const void* E, const void* Dw, void* Z, int64_t T, int32_t d,
@@ -137,9 +158,9 @@ dv_status dv_build_visual_memory(const void* E, const void* Dw, void* Z, int64_t
   DV_CHECK(need_ptr(E, "E"));
   DV_CHECK(need_ptr(Dw, "Dw"));
   DV_CHECK(need_ptr(Z, "Z"));
-  return hip_status(dv::launch_down_act(E, Dw, Z, T, d, L, r, act, dtype == DV_BF16 ? 1 : 0,
-                                        (hipStream_t)stream, g_ev),
-                    "dv_build_visual_memory launch");
+  return launched(dv::launch_down_act(E, Dw, Z, T, d, L, r, act, dtype == DV_BF16 ? 1 : 0,
+                                      (hipStream_t)stream, g_ev),
+                  "dv_build_visual_memory launch", (hipStream_t)stream);
 }
 
 size_t dv_project_visual_kv_workspace(int64_t T, int32_t d, int32_t nl, int32_t dtype) {
@@ -236,7 +257,7 @@ dv_status project_impl(const void* E, const void* Z, const void* Uw, const void*
                                          ea.any() ? &ea : nullptr);
     if (e != hipSuccess) return hip_status(e, name);
   }
-  return ok();
+  return launched(hipSuccess, name, stream);
 }
 
 }  // namespace
@@ -309,10 +330,10 @@ dv_status dv_recurrent_visual_kv(const void* E, const void* Dw, const void* Uw, 
     return fail(DV_ERR_WORKSPACE, "workspace of %zu bytes is below the required %zu",
                 ws ? ws_bytes : (size_t)0, w.bytes);
   if (!aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
-  return hip_status(dv::launch_recurrent(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv, B, Nv, d, L, r, Hkv,
-                                         hd, act, eps, dtype == DV_BF16 ? 1 : 0, ws, w,
-                                         (hipStream_t)stream, g_ev),
-                    "dv_recurrent_visual_kv launch");
+  return launched(dv::launch_recurrent(E, Dw, Uw, gamma, Wk, Wv, Kv, Vv, B, Nv, d, L, r, Hkv,
+                                       hd, act, eps, dtype == DV_BF16 ? 1 : 0, ws, w,
+                                       (hipStream_t)stream, g_ev),
+                  "dv_recurrent_visual_kv launch", (hipStream_t)stream);
 }
 
 // Z of the kept layers (call dtype, 256-byte aligned) followed by the projection slots.
@@ -399,7 +420,7 @@ dv_status dv_kept_visual_kv(const void* E, const void* Dw, const void* Uw, const
     c += n;
     a = b;
   }
-  return ok();
+  return launched(hipSuccess, "dv_kept_visual_kv launch", s);
 }
 
 size_t dv_delta_rule_workspace(int32_t B, int32_t Hv, int32_t N, int32_t dk, int32_t dv,
@@ -434,9 +455,9 @@ dv_status dv_delta_rule_write(const void* k, const void* v, const float* alpha, 
                 ws ? ws_bytes : (size_t)0, need);
   if (!aligned16(ws)) return fail(DV_ERR_ALIGN, "ws is not 16-byte aligned");
   const dv::GdrWs w = dv::gdr_layout(ws, B, Hv, N, dk, dv, bf);
-  return hip_status(dv::launch_delta_rule(k, v, alpha, beta, S, B, Hk, Hv, N, dk, dv, bf, w,
-                                          (hipStream_t)stream, g_ev),
-                    "dv_delta_rule_write launch");
+  return launched(dv::launch_delta_rule(k, v, alpha, beta, S, B, Hk, Hv, N, dk, dv, bf, w,
+                                        (hipStream_t)stream, g_ev),
+                  "dv_delta_rule_write launch", (hipStream_t)stream);
 }
 
 size_t dv_text_visual_attention_workspace(int32_t B, int32_t Hq, int32_t Hkv, int32_t hd,
@@ -515,7 +536,8 @@ dv_status run_attention(const void* Q, const void* Kv, const void* Vv, const voi
   a.splits = plan.splits;
   a.keys_per_split = plan.keys_per_split;
   a.tiles_per_split = plan.tiles_per_split;
-  return hip_status(dv::launch_attention(a, plan, dtype == DV_BF16 ? 1 : 0, stream, g_ev), name);
+  return launched(dv::launch_attention(a, plan, dtype == DV_BF16 ? 1 : 0, stream, g_ev), name,
+                  stream);
 }
 
 }  // namespace

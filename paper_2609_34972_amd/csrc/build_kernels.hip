@@ -219,7 +219,8 @@ __global__ __launch_bounds__(C::NT) void k_kv_proj(const typename C::elem* __res
 
 // ---------------------------------------------------------------- bf16 pipelined kernels
 
-typedef PipeCfg<128, 128, 2, 2> DownP;  // 2304 x 8192 at LLaVA shapes: 1152 tiles
+typedef PipeCfg<128, 128, 2, 2> DownP;  // two blocks per CU
+typedef PipeCfg<96, 128, 2, 2> DownP96;  // two blocks per CU; 2304 x 8192: 1536 tiles, 3 rounds
 typedef PipeCfg<128, 128, 2, 2> UpP;    // K = r is short; two blocks per CU overlap epilogues
 typedef PipeCfg<256, 256, 4, 2> KvP;    // 9216 tiles of 256 x 256 over 32 LLaVA layers
 // K/V epilogue staging: per wave 64 rows of 128 bf16, rows padded by 16 B.
@@ -759,6 +760,14 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
     (void)once;
     const int64_t N = (int64_t)L * r;
     const bool big = cdiv(N, KvP::BN) * cdiv(T_, KvP::BM) >= 4 * 256;
+    // Below that, 128 x 128 or 96 x 128 tiles, whichever needs fewer tile-rounds of the 512
+    // block slots, counting a 96-row tile as 0.8 of a 128-row one (its loads and fragment reads
+    // per MFMA are higher): LLaVA-7B's 2304 x 8192 takes 3 rounds of 96 x 128 tiles against 2.25
+    // (so 3) rounds of 128 x 128 ones.
+    const int64_t slots = 2 * 256;
+    const int64_t r128 = cdiv(cdiv(N, DownP::BN) * cdiv(T_, DownP::BM), slots);
+    const int64_t r96 = cdiv(cdiv(N, DownP96::BN) * cdiv(T_, DownP96::BM), slots);
+    const bool rows96 = !big && 10 * r96 * 96 < 8 * r128 * 128;
     record(ev.down[0], s);
     if (big) {
       dim3 grid(cdiv(N, KvP::BN), cdiv(T_, KvP::BM));
@@ -768,6 +777,14 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
       else
         k_down_act_p<KvP, 1><<<grid, dim3(KvP::NT), KvP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
                                                                          (bf16*)Z, (int)T_, d, L, r);
+    } else if (rows96) {
+      dim3 grid(cdiv(N, DownP96::BN), cdiv(T_, DownP96::BM));
+      if (act == 0)
+        k_down_act_p<DownP96, 0><<<grid, dim3(DownP96::NT), DownP96::LDS_BYTES, s>>>(
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
+      else
+        k_down_act_p<DownP96, 1><<<grid, dim3(DownP96::NT), DownP96::LDS_BYTES, s>>>(
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
     } else {
       dim3 grid(cdiv(N, DownP::BN), cdiv(T_, DownP::BM));
       if (act == 0)

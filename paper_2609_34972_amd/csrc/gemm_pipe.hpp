@@ -112,26 +112,32 @@ __device__ __forceinline__ PipeLoads<C> pipe_loads(const BufOperand& A, const Bu
   return p;
 }
 
-// Each wave issues A_INS + B_INS 1 KiB loads (8 rows x 128 bytes) of one 64-deep K tile. With
-// an even count per wave, a load's block parity (which selects the swizzle key half) is that of
-// its index.
+// Each wave issues A_INS + B_INS 1 KiB loads (8 rows x 128 bytes) of one 64-deep K tile. A
+// load's 8-row block parity selects the swizzle key half; with an even count per wave it is that
+// of the load's index, with an odd count it also depends on the wave.
+template <int INS>
+__device__ __forceinline__ bool pipe_odd_block(int wave, int i) {
+  return INS % 2 == 0 ? (i & 1) != 0 : ((wave * INS + i) & 1) != 0;
+}
+
 template <class C>
 __device__ __forceinline__ void pipe_issue(const PipeLoads<C>& p, int kbytes, bf16* stage, int va0,
                                            int va1, int vb0, int vb1) {
-  static_assert(C::A_INS % 2 == 0 && C::B_INS % 2 == 0, "block parity must follow the index");
   const int wave = wave_index();
 #pragma unroll
   for (int i = 0; i < C::A_INS; ++i) {
     const int blk = wave * C::A_INS + i;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(p.ra, (lds_void*)(stage + blk * 512), 16,
-                                             (i & 1) ? va1 : va0, p.sa[i] + kbytes, 0, 0);
+                                             pipe_odd_block<C::A_INS>(wave, i) ? va1 : va0,
+                                             p.sa[i] + kbytes, 0, 0);
   }
   bf16* sb = stage + C::BM * C::BK;
 #pragma unroll
   for (int i = 0; i < C::B_INS; ++i) {
     const int blk = wave * C::B_INS + i;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(p.rb[i].r, (lds_void*)(sb + blk * 512), 16,
-                                             (i & 1) ? vb1 : vb0, p.sb[i] + kbytes, 0, 0);
+                                             pipe_odd_block<C::B_INS>(wave, i) ? vb1 : vb0,
+                                             p.sb[i] + kbytes, 0, 0);
   }
 }
 
@@ -196,21 +202,25 @@ __device__ __forceinline__ void pipe_step0_pattern() {
 // Issue order of the second K step: the refill loads first, each followed by kPer MFMAs (loads
 // spread out went slightly faster than one per MFMA; fragment reads first, slower), then each of
 // the next tile's fragment reads followed by one MFMA, then the rest of the MFMAs.
+// Tiles with fewer MFMAs per K step than loads plus reads (e.g. 96 x 128) leave the order to the
+// compiler.
 template <class C>
 __device__ __forceinline__ void pipe_step1_pattern() {
   constexpr int kPer = (C::FM * C::FN - (C::FM + C::FN)) / C::INS;
-  static_assert(kPer >= 1, "one MFMA per load and per read");
+  if constexpr (kPer >= 1) {
 #pragma unroll
-  for (int i = 0; i < C::INS; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
-    __builtin_amdgcn_sched_group_barrier(0x008, kPer, 1);
-  }
+    for (int i = 0; i < C::INS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, kPer, 1);
+    }
 #pragma unroll
-  for (int i = 0; i < C::FM + C::FN; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    for (int i = 0; i < C::FM + C::FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008,
+                                         C::FM * C::FN - kPer * C::INS - (C::FM + C::FN), 1);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN - kPer * C::INS - (C::FM + C::FN), 1);
 }
 
 // A: block-tile rows start at A's first row; B likewise. K must be a multiple of 64.
