@@ -317,11 +317,23 @@ def make_step(w, Eg, wg, tg, buf):
     return step
 
 
+def fused_path(w) -> bool:
+    """Whether this workload's projection takes the fused up + norm + K/V kernel (then the K/V
+    events bracket that kernel and the up-projection events record nothing)."""
+    import torch
+
+    import paper_2609_34972_amd as dvl
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    return dvl.project_visual_kv_fused(w.d, w.r, w.Hkv, w.hd, dt)
+
+
 def measure_step(w, step, steps, warmup, n_attn_steps=3):
     """Time `steps` whole steps (the three build launches bracketed by HIP events inside the
     timed region), then time the attention launches in `n_attn_steps` extra steps: events
     between the 32 short attention launches would add gaps to the timed steps."""
     import torch
+
+    fused = fused_path(w)
 
     for _ in range(warmup):
         step()
@@ -345,8 +357,8 @@ def measure_step(w, step, steps, warmup, n_attn_steps=3):
         step(attn_ev=attn_evs[s])
     torch.cuda.synchronize()
     avg = lambda key: sum(hev.ms(e[key]) for e in evs) / steps
-    m = {"ms_step": t_begin.elapsed_time(t_end) / steps, "step_ms": step_ms,
-         "down": avg("down"), "up": avg("up"), "kv": avg("kv"),
+    m = {"ms_step": t_begin.elapsed_time(t_end) / steps, "step_ms": step_ms, "fused": fused,
+         "down": avg("down"), "up": 0.0 if fused else avg("up"), "kv": avg("kv"),
          "attn_launch": sum(hev.ms(a) for e in attn_evs for a in e) / (n_attn_steps * w.L)}
     hev.close()
     return m
@@ -365,9 +377,13 @@ def step_figures(w, m, peak):
     ms_build = m["down"] + m["up"] + m["kv"]
     ms_attn_total = m["ms_step"] - ms_build
     ms_al = m["attn_launch"]
+    fused = m.get("fused", False)
+    # the fused kernel does the up-projection's work too
+    f_kv_kernel = f_kv + f_up if fused else f_kv
     return {
-        "f_kv": f_kv, "f_build": f_build, "f_attn": f_attn,
-        "kv_tflops": f_kv / (m["kv"] * 1e-3) / 1e12,
+        "f_kv": f_kv_kernel, "f_build": f_build, "f_attn": f_attn, "fused": fused,
+        "kv_kernel": "k_up_kv_fused" if fused else "k_kv_proj",
+        "kv_tflops": f_kv_kernel / (m["kv"] * 1e-3) / 1e12,
         "stages": {
             "build_kv_visual_tokens_per_s": w.T / (ms_build * 1e-3),
             "build_kv_ms": ms_build,
@@ -375,8 +391,8 @@ def step_figures(w, m, peak):
             "build_kv_mfma_frac": f_build / (ms_build * 1e-3) / 1e12 / peak,
             "down_ms": m["down"], "up_ms": m["up"], "kv_ms": m["kv"],
             "down_mfma_frac": f_down / (m["down"] * 1e-3) / 1e12 / peak,
-            "up_mfma_frac": f_up / (m["up"] * 1e-3) / 1e12 / peak,
-            "kv_mfma_frac": f_kv / (m["kv"] * 1e-3) / 1e12 / peak,
+            "up_mfma_frac": None if fused else f_up / (m["up"] * 1e-3) / 1e12 / peak,
+            "kv_mfma_frac": f_kv_kernel / (m["kv"] * 1e-3) / 1e12 / peak,
             "attention_ms_all_layers": ms_attn_total,
             "attention_kernel_ms_per_layer": ms_al,
             "attention_tflops": f_attn / (ms_attn_total * 1e-3) / 1e12,
@@ -426,7 +442,7 @@ def run_prefill(args, w):
         "config": {"workload": w.name, "batch": w.B, "visual_tokens": w.Nv, "text_tokens": w.Nt,
                    "layers": w.L, "d": w.d, "rank": w.r, "q_heads": w.Hq, "kv_heads": w.Hkv,
                    "head_dim": w.hd},
-        "roofline": {"bound": "mfma", "kernel": "k_kv_proj", "achieved": kv_tflops, "peak": peak,
+        "roofline": {"bound": "mfma", "kernel": fig["kv_kernel"], "achieved": kv_tflops, "peak": peak,
                      "unit": "TFLOP/s", "frac": kv_tflops / peak,
                      "traffic": stored_traffic() if w.name == "llava7b" else None,
                      "algorithmic_flops_per_launch": fig["f_kv"], "ms_per_launch": m["kv"]},
@@ -490,8 +506,9 @@ def run_workload_block(args, w):
         "visual_tokens_per_s": w.T / (m["ms_step"] * 1e-3),
         "step_mfma_frac": st["step_mfma_frac"],
         "build_kv_ms": st["build_kv_ms"], "build_kv_mfma_frac": st["build_kv_mfma_frac"],
-        "down_ms": st["down_ms"], "up_ms": st["up_ms"],
-        "k_kv_proj": {"ms": m["kv"], "tflops": fig["kv_tflops"], "frac": fig["kv_tflops"] / peak},
+        "down_ms": st["down_ms"], "up_ms": st["up_ms"], "fused_up_kv": fig["fused"],
+        "k_kv_proj": {"kernel": fig["kv_kernel"], "ms": m["kv"], "tflops": fig["kv_tflops"],
+                      "frac": fig["kv_tflops"] / peak},
         "attention": {"kernel_ms_per_layer": m["attn_launch"],
                       "bound": "mfma" if mfma_bound else "hbm",
                       "frac": st["attention_kernel_mfma_frac"] if mfma_bound
@@ -500,6 +517,22 @@ def run_workload_block(args, w):
                       "gbs": st["attention_kernel_gbs"],
                       "ms_all_layers_in_step": st["attention_ms_all_layers"]},
     }
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    import paper_2609_34972_amd as dvl
+    dvl.set_fused_kv(True)
+    try:
+        if dvl.project_visual_kv_fused(w.d, w.r, w.Hkv, w.hd, dt):
+            # the fused up + norm + K/V kernel (off by default), timed on the same inputs
+            log(f"[bench] {w.name}: timing the fused up + norm + K/V variant")
+            mf = measure_step(w, step, max(3, steps // 2), 1, n_attn_steps=1)
+            ff = step_figures(w, mf, peak)
+            res["fused_up_kv_variant"] = {
+                "ms_per_step": mf["ms_step"], "build_kv_ms": ff["stages"]["build_kv_ms"],
+                "kernel": ff["kv_kernel"], "kernel_ms": mf["kv"], "tflops": ff["kv_tflops"],
+                "frac": ff["kv_tflops"] / peak,
+                "vs_default_up_plus_kv_ms": m["up"] + m["kv"]}
+    finally:
+        dvl.set_fused_kv(False)
     del x, Eg, tg, wg, buf, step
     torch.cuda.empty_cache()
     return res

@@ -88,6 +88,11 @@ dv_status dv_build_visual_memory(const void* E, const void* Dw, void* Z, int64_t
  *         With room for k layers the call processes layers in groups of up to k;
  *         dv_project_visual_kv_workspace(B*Nv, d, nl, dtype) holds all of them at once.
  * M_l is transient (it lives only in the workspace), as the method prescribes.
+ * Narrow K/V widths can take one fused kernel instead (dv_set_fused_kv): it keeps M_l of 64
+ * tokens on chip and projects it at once, so the workspace is validated but not used. Its
+ * rounding points are the same (M_l in fp32, M_l * gamma_l rounded to the call dtype before the
+ * projection, the row scale applied to the fp32 product); only the order in which the row sum
+ * of squares and the products over d are added up differs.
  */
 size_t dv_project_visual_kv_workspace(int64_t T, int32_t d, int32_t nl, int32_t dtype);
 dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, const void* gamma,
@@ -95,6 +100,23 @@ dv_status dv_project_visual_kv(const void* E, const void* Z, const void* Uw, con
                                int32_t Nv, int32_t d, int32_t L, int32_t r, int32_t Hkv,
                                int32_t hd, int32_t l0, int32_t nl, float eps, int32_t dtype,
                                void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Fused up-projection + RMSNorm + K/V kernel for narrow K/V widths: bf16, 2 * Hkv * hd = 1024
+ * (e.g. 4 K/V heads of 128), r in {128, 256, 512}, d a multiple of 64. The 64 x 1024 fp32 K/V
+ * accumulators of a block fit in registers, so M_l is computed once per token and never
+ * written out. It is off by default: each block of 64 tokens reads the layer's whole U_l and
+ * [Wk | Wv] from the L2, about 1.4 times the L2-to-CU traffic of the two-kernel path, and on
+ * MI355X at the Qwen2.5-VL video shape it measured slower than that path despite saving the
+ * workspace round trip.
+ *   dv_set_fused_kv(1) makes dv_project_visual_kv, dv_project_visual_kv_ex with no epilogue
+ *   step and dv_kept_visual_kv take it for those sizes; dv_set_fused_kv(0) restores the
+ *   default. Process-wide; a call already enqueued keeps its kernel. on must be 0 or 1.
+ *   dv_project_visual_kv_fused returns 1 when a call with these sizes takes the fused kernel
+ *   under the current setting, else 0 (also for any size the projection rejects); no GPU work.
+ */
+dv_status dv_set_fused_kv(int32_t on);
+int32_t dv_project_visual_kv_fused(int32_t d, int32_t r, int32_t Hkv, int32_t hd, int32_t dtype);
 
 /*
  * Recurrent adapter (Section 3.1, Eq. 6) and the visual K/V projection (Section 3.2, Eq. 7) of
@@ -261,7 +283,9 @@ dv_status dv_delta_rule_write(const void* k, const void* v, const float* alpha, 
  *                        whole per-layer adapter chain of dv_recurrent_visual_kv
  *   DV_KERNEL_UP         the up-projection + residual of dv_project_visual_kv
  *   DV_KERNEL_KV         the RMSNorm-scaled K/V projection of dv_project_visual_kv and
- *                        dv_recurrent_visual_kv
+ *                        dv_recurrent_visual_kv; when dv_project_visual_kv takes the fused
+ *                        kernel, that kernel, which also does the up-projection
+ *                        (DV_KERNEL_UP then records nothing)
  *   DV_KERNEL_ATTENTION  the main attention kernel of dv_text_visual_attention
  *                        (without the split-merge kernel)
  *   DV_KERNEL_DELTA_PREP the per-chunk preparation of dv_delta_rule_write

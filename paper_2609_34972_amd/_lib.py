@@ -26,6 +26,8 @@ EXPORTS = (
     "dv_build_visual_memory",
     "dv_project_visual_kv_workspace",
     "dv_project_visual_kv",
+    "dv_project_visual_kv_fused",
+    "dv_set_fused_kv",
     "dv_text_visual_attention_workspace",
     "dv_text_visual_attention",
     "dv_text_visual_attention_noalloc",
@@ -98,6 +100,10 @@ def load() -> ctypes.CDLL:
         lib.dv_project_visual_kv_workspace.restype = sz
         lib.dv_project_visual_kv.argtypes = [vp] * 8 + [i32] * 9 + [f32, i32, vp, sz, vp]
         lib.dv_project_visual_kv.restype = i32
+        lib.dv_project_visual_kv_fused.argtypes = [i32] * 5
+        lib.dv_project_visual_kv_fused.restype = i32
+        lib.dv_set_fused_kv.argtypes = [i32]
+        lib.dv_set_fused_kv.restype = i32
         lib.dv_project_visual_kv_ex_workspace.argtypes = [i64, i32, i32, i32, i32]
         lib.dv_project_visual_kv_ex_workspace.restype = sz
         lib.dv_project_visual_kv_ex.argtypes = ([vp] * 8 + [i32] * 9 + [f32, ctypes.POINTER(_KvEpilogue), i32, vp, sz, vp])
@@ -212,6 +218,18 @@ def build_visual_memory(E: torch.Tensor, Dw: torch.Tensor, Z: torch.Tensor, act:
 def project_visual_kv_workspace(T: int, d: int, nl: int, dtype: torch.dtype) -> int:
     code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
     return int(load().dv_project_visual_kv_workspace(T, d, nl, code))
+
+
+def project_visual_kv_fused(d: int, r: int, Hkv: int, hd: int, dtype: torch.dtype) -> bool:
+    """Whether project_visual_kv (no epilogue) takes the fused up + norm + K/V kernel now."""
+    code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
+    return bool(load().dv_project_visual_kv_fused(d, r, Hkv, hd, code))
+
+
+def set_fused_kv(on: bool) -> None:
+    """Switch the fused up + norm + K/V kernel on or off for the sizes it covers (process-wide;
+    off by default)."""
+    _check(load().dv_set_fused_kv(1 if on else 0))
 
 
 def project_visual_kv_ex_workspace(T: int, d: int, nl: int, hd: int, dtype: torch.dtype) -> int:

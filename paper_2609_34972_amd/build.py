@@ -18,7 +18,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdeltavision.so")
 INFO = os.path.join(HERE, "build_info.json")
 SOURCES = ["api.cpp", "build_kernels.hip", "attention.hip", "recurrent.hip", "delta_rule.hip",
-           "probe.hip"]
+           "probe.hip", "fused_kv.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

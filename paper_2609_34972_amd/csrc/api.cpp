@@ -168,6 +168,17 @@ size_t dv_project_visual_kv_workspace(int64_t T, int32_t d, int32_t nl, int32_t 
   return (size_t)nl * kv_ws_layer_bytes(T, d, dtype);
 }
 
+int32_t dv_project_visual_kv_fused(int32_t d, int32_t r, int32_t Hkv, int32_t hd, int32_t dtype) {
+  if (d <= 0 || r <= 0 || Hkv <= 0 || hd <= 0 || (dtype != DV_F32 && dtype != DV_BF16)) return 0;
+  return dv::up_kv_fused(d, r, Hkv, hd, dtype == DV_BF16 ? 1 : 0, false) ? 1 : 0;
+}
+
+dv_status dv_set_fused_kv(int32_t on) {
+  if (on != 0 && on != 1) return fail(DV_ERR_SHAPE, "on must be 0 or 1 (got %d)", on);
+  dv::set_up_kv_fused(on != 0);
+  return ok();
+}
+
 }  // extern "C"
 
 namespace {

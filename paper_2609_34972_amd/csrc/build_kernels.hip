@@ -229,6 +229,33 @@ constexpr int kKvEpiBytes = KvP::NWAVES * KvP::WM * kKvEpiPitch;
 constexpr int kKvRsOffset = KvP::LDS_BYTES > kKvEpiBytes ? KvP::LDS_BYTES : kKvEpiBytes;
 constexpr int kKvLdsBytes = kKvRsOffset + KvP::BM * 4;  // + row scales
 
+// Output tile (row tile mt, column tile nt) of a block when the tiles of one XCD should form
+// compact supertiles. The dispatcher deals consecutive workgroup ids out to the 8 XCDs in turn, so
+// in launch order (column tile fastest) every XCD touches every row tile and the blocks that share
+// an operand tile sit on different L2s. Here the ids of each XCD (id % 8) are renumbered to be
+// consecutive, XCD x taking the x-th eighth of the tile sequence, and the sequence walks bands of
+// sh row tiles, each band in sh x sw supertiles (row within the supertile slowest). The blocks an
+// XCD holds at once then share a few row tiles and a few column tiles of the two operands. Ids past
+// the last multiple of 8 keep their place; sh == 0 keeps launch order. Grid x = column tiles,
+// y = row tiles; z (layers) is left to the caller.
+struct Tile2 {
+  int mt, nt;
+};
+__device__ __forceinline__ Tile2 supertile_order(int sh, int sw) {
+  if (sh == 0) return Tile2{(int)blockIdx.y, (int)blockIdx.x};
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int id = blockIdx.x + gx * blockIdx.y;
+  const int per = gx * gy / 8, full = per * 8;
+  const int q = id < full ? (id % 8) * per + id / 8 : id;
+  const int band = q / (sh * gx);
+  const int h = min(sh, gy - band * sh);
+  const int in = q - band * sh * gx;
+  const int cs = in / (h * sw);
+  const int w = min(sw, gx - cs * sw);
+  const int j = in - cs * h * sw;
+  return Tile2{band * sh + j / w, cs * sw + j % w};
+}
+
 template <typename F>
 __device__ __forceinline__ void store4_bf16(bf16* p, float a, float b, float c, float d, F f) {
   bf16x4 v = {(bf16)f(a), (bf16)f(b), (bf16)f(c), (bf16)f(d)};
@@ -245,10 +272,11 @@ template <class C, int ACT>
 __global__ __launch_bounds__(C::NT) void k_down_act_p(const bf16* __restrict__ E,
                                                       const bf16* __restrict__ Dw,
                                                       bf16* __restrict__ Z, int T, int d, int L,
-                                                      int r) {
+                                                      int r, int sh, int sw) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int N = L * r;
-  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const Tile2 tile = supertile_order(sh, sw);
+  const int n0 = tile.nt * C::BN, m0 = tile.mt * C::BM;
   const int ldb = d * 2;
   BufOperand A{buffer_rsrc(E + (int64_t)m0 * d, (int64_t)(T - m0) * ldb),
                buffer_rsrc(E, 0), 1 << 30, ldb};
@@ -277,10 +305,13 @@ __global__ __launch_bounds__(C::NT) void k_down_act_p(const bf16* __restrict__ E
 
 // Up-projection epilogue scratch past the two stages: per wave a 16 x 64 bf16 transpose buffer
 // (rows padded by 16 bytes), then the per-row sums of squares of the two column halves.
-constexpr int kUpScrPitch = UpP::WN + 8;  // bf16 elements
-constexpr int kUpScrOffset = UpP::LDS_BYTES;
-constexpr int kUpSsOffset = kUpScrOffset + UpP::NWAVES * 16 * kUpScrPitch * 2;
-constexpr int kUpLdsBytes = kUpSsOffset + UpP::WGN * UpP::BM * 4;
+template <class C>
+struct UpLds {
+  static constexpr int SCR_PITCH = C::WN + 8;  // bf16 elements
+  static constexpr int SCR = C::LDS_BYTES;
+  static constexpr int SS = SCR + C::NWAVES * 16 * SCR_PITCH * 2;
+  static constexpr int BYTES = SS + C::WGN * C::BM * 4;
+};
 
 // Layers per block of the up projection: the block's tile of E is read once for all of them.
 constexpr int kUpLayers = 4;
@@ -299,10 +330,11 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        const bf16* __restrict__ gamma,
                                                        bf16* __restrict__ Mg,
                                                        float* __restrict__ ssq, int T, int d,
-                                                       int r, int l0, int nl) {
+                                                       int r, int l0, int nl, int sh, int sw) {
   static_assert(C::WGN == 2 && C::WN == 64, "epilogue assumes two 64-column wave halves");
   extern __shared__ __align__(16) unsigned char smem[];
-  const int n0 = blockIdx.x * C::BN, m0 = blockIdx.y * C::BM;
+  const Tile2 tile = supertile_order(sh, sw);
+  const int n0 = tile.nt * C::BN, m0 = tile.mt * C::BM;
   const int lz0 = blockIdx.z * kUpLayers, nrun = min(nl - lz0, kUpLayers);
   const int ldb = r * 2;
   const int lane = threadIdx.x & 63, wave = wave_index();
@@ -326,8 +358,9 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
   };
   u32x2 g4[C::FN];
   load_gamma(lz0, g4);
-  bf16* scr = (bf16*)(smem + kUpScrOffset) + wave * 16 * kUpScrPitch;
-  float* ssx = (float*)(smem + kUpSsOffset);
+  constexpr int kUpScrPitch = UpLds<C>::SCR_PITCH;
+  bf16* scr = (bf16*)(smem + UpLds<C>::SCR) + wave * 16 * kUpScrPitch;
+  float* ssx = (float*)(smem + UpLds<C>::SS);
   const int np = (d + C::BN - 1) / C::BN;
 
   auto operands = [&](int run, BufOperand& A, BufOperand& B) {
@@ -394,7 +427,7 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
     if (threadIdx.x < C::BM) {
       const int row = m0 + threadIdx.x;
       if (row < T)
-        ssq[((int64_t)lz * np + blockIdx.x) * T + row] = ssx[threadIdx.x] + ssx[C::BM + threadIdx.x];
+        ssq[((int64_t)lz * np + tile.nt) * T + row] = ssx[threadIdx.x] + ssx[C::BM + threadIdx.x];
     }
   };
   pipe_runs<C>(nrun, r, (bf16*)smem, operands, epilogue);
@@ -731,6 +764,13 @@ static void allow_lds(K kernel, int bytes) {
 
 // ---------------------------------------------------------------- launchers
 
+// Supertile shapes of the pipelined down and up projections (see supertile_order).
+struct TileOrder {
+  int sh, sw;
+};
+static TileOrder down_order() { return TileOrder{8, 8}; }
+static TileOrder up_order() { return TileOrder{8, 8}; }
+
 static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 template <typename T>
@@ -768,31 +808,32 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
     const int64_t r128 = cdiv(cdiv(N, DownP::BN) * cdiv(T_, DownP::BM), slots);
     const int64_t r96 = cdiv(cdiv(N, DownP96::BN) * cdiv(T_, DownP96::BM), slots);
     const bool rows96 = !big && 10 * r96 * 96 < 8 * r128 * 128;
+    const TileOrder ord = down_order();
     record(ev.down[0], s);
     if (big) {
       dim3 grid(cdiv(N, KvP::BN), cdiv(T_, KvP::BM));
       if (act == 0)
         k_down_act_p<KvP, 0><<<grid, dim3(KvP::NT), KvP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
-                                                                         (bf16*)Z, (int)T_, d, L, r);
+                                                                         (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
       else
         k_down_act_p<KvP, 1><<<grid, dim3(KvP::NT), KvP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
-                                                                         (bf16*)Z, (int)T_, d, L, r);
+                                                                         (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
     } else if (rows96) {
       dim3 grid(cdiv(N, DownP96::BN), cdiv(T_, DownP96::BM));
       if (act == 0)
         k_down_act_p<DownP96, 0><<<grid, dim3(DownP96::NT), DownP96::LDS_BYTES, s>>>(
-            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
       else
         k_down_act_p<DownP96, 1><<<grid, dim3(DownP96::NT), DownP96::LDS_BYTES, s>>>(
-            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
     } else {
       dim3 grid(cdiv(N, DownP::BN), cdiv(T_, DownP::BM));
       if (act == 0)
         k_down_act_p<DownP, 0><<<grid, dim3(DownP::NT), DownP::LDS_BYTES, s>>>(
-            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
       else
         k_down_act_p<DownP, 1><<<grid, dim3(DownP::NT), DownP::LDS_BYTES, s>>>(
-            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r);
+            (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
     }
     record(ev.down[1], s);
     return hipGetLastError();
@@ -861,17 +902,26 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
   static bool once = [] {
     allow_lds(k_kv_proj_p<false>, kv_lds);
     allow_lds(k_kv_proj_p<true>, kv_lds);
-    allow_lds(k_up_norm_p<UpP>, kUpLdsBytes);
+    allow_lds(k_up_norm_p<UpP>, UpLds<UpP>::BYTES);
     return true;
   }();
   (void)once;
+  if (up_kv_fused(d, r, Hkv, hd, 1, epi && epi->any())) {
+    // M, its norm and the projection in one kernel (timed as the K/V projection)
+    if (first) record(ev.kv[0], s);
+    const hipError_t e = launch_up_kv_fused(E, Z, Uw, gamma, Wk, Wv, Kv, Vv, B_, Nv, d, r, Hkv,
+                                            hd, l0, nl, eps, s);
+    if (last) record(ev.kv[1], s);
+    return e;
+  }
   const int T_ = B_ * Nv;
   const int np = cdiv(d, UpP::BN);
   dim3 gu(np, cdiv(T_, UpP::BM), cdiv(nl, kUpLayers));
+  const TileOrder uo = up_order();
   if (first) record(ev.up[0], s);
-  k_up_norm_p<UpP><<<gu, dim3(UpP::NT), kUpLdsBytes, s>>>(
+  k_up_norm_p<UpP><<<gu, dim3(UpP::NT), UpLds<UpP>::BYTES, s>>>(
       (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_, d, r,
-      l0, nl);
+      l0, nl, uo.sh, uo.sw);
   if (last) record(ev.up[1], s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -59,6 +59,18 @@ hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const
                              void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
                              bool first_group, bool last_group, const KvEpiArgs* epi = nullptr);
 
+// The fused kernel (fused_kv.hip) computes M_l, its RMSNorm and the K/V projection of 64 tokens
+// in one block and needs no workspace. It covers bf16, 2 Hkv hd = 1024, r in {128, 256, 512},
+// d a multiple of 64, no backbone epilogue (up_kv_fused_eligible), and the projection takes it
+// only once switched on (set_up_kv_fused; off at load).
+bool up_kv_fused_eligible(int d, int r, int Hkv, int hd, int dtype);
+void set_up_kv_fused(bool on);
+bool up_kv_fused(int d, int r, int Hkv, int hd, int dtype, bool epilogue);
+hipError_t launch_up_kv_fused(const void* E, const void* Z, const void* Uw, const void* gamma,
+                              const void* Wk, const void* Wv, void* Kv, void* Vv, int B, int Nv,
+                              int d, int r, int Hkv, int hd, int l0, int nl, float eps,
+                              hipStream_t s);
+
 // K/V projection alone (Eq. 7) for layers l0..l0+nl-1 from a prepared workspace: Mg holds
 // M_l * gamma_l for each layer of the range (call dtype) and ssq np partial sums of M_l^2 per row.
 hipError_t launch_kv_only(const void* Mg, const float* ssq, const void* Wk, const void* Wv,

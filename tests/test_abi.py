@@ -111,6 +111,27 @@ def attn_call(lib, ws=None, ws_bytes=0, **over):
                                         a["q0"], a["scale"], a["dt"], ws, ws_bytes, None)
 
 
+def test_project_visual_kv_fused_rule(lib):
+    """The fused up + norm + K/V kernel covers bf16 with 2 Hkv hd = 1024, r in {128, 256, 512}
+    and d a multiple of 64, and is taken only while switched on."""
+    eligible = [(3584, 512, 4, 128, BF16), (384, 256, 8, 64, BF16), (192, 128, 4, 128, BF16)]
+    other = [(3584, 512, 4, 128, F32),        # fp32
+             (4096, 256, 32, 128, BF16),      # K/V width 8192
+             (3584, 384, 4, 128, BF16),       # rank 384
+             (3584, 64, 4, 128, BF16),        # rank 64
+             (3552, 512, 4, 128, BF16),       # d % 64 != 0
+             (0, 512, 4, 128, BF16), (3584, 512, 1 << 30, 128, BF16), (3584, 512, 4, 128, 9)]
+    assert all(lib.dv_project_visual_kv_fused(*a) == 0 for a in eligible + other)  # off at load
+    assert lib.dv_set_fused_kv(2) == SHAPE
+    try:
+        assert lib.dv_set_fused_kv(1) == 0
+        assert all(lib.dv_project_visual_kv_fused(*a) == 1 for a in eligible)
+        assert all(lib.dv_project_visual_kv_fused(*a) == 0 for a in other)
+    finally:
+        assert lib.dv_set_fused_kv(0) == 0
+    assert all(lib.dv_project_visual_kv_fused(*a) == 0 for a in eligible)
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(Q=None), NULL), (dict(Kt=None), NULL), (dict(O=None), NULL), (dict(Kv=None), NULL),
     (dict(Vt=FAKE + 4), ALIGN),

@@ -54,6 +54,8 @@ BUILD = [
     # GQA, hd 64, d not a multiple of the column tile, 3 x 37 tokens
     configs.QWEN25VL_VIDEO.with_(name="g_gqa_hd64", d=960, L=3, r=64, Hq=8, Hkv=2, hd=64, B=3,
                                  Nv=37, Nt=16),
+    # K/V width 1024, rank 128, 100 tokens: ragged row tiles (run with the fused kernel too)
+    configs.QWEN25VL_VIDEO.with_(name="g_fused_r128", d=320, L=2, r=128, B=1, Nv=100),
     # fp32 engine
     configs.TINY.with_(name="g_f32", d=320, L=3, r=48, Hq=6, Hkv=3, hd=128, B=2, Nv=35,
                        act=configs.ACT_SILU),
@@ -63,6 +65,15 @@ BUILD = [
 @pytest.mark.parametrize("w", BUILD, ids=lambda w: w.name)
 def test_build_and_projection_stay_inside(w):
     say(f"[guard build {w.name}]")
+    fused = w.name.startswith("g_fused")
+    dvl.set_fused_kv(fused)
+    try:
+        _build_and_projection(w)
+    finally:
+        dvl.set_fused_kv(False)
+
+
+def _build_and_projection(w):
     E, wts = synth.make_E(w, 9), synth.make_build_weights(w, 9)
     Eg, wg = cuda(E), {k: cuda(v) for k, v in wts.items()}
     dt = Eg.dtype
