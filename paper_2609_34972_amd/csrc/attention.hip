@@ -301,7 +301,30 @@ __device__ __forceinline__ int key_v(int row) { return (row & 7) << 1; }
 }  // namespace stream
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// Transposed LDS reads of V (ds_read_b64_tr_b16) issued as inline assembly. The compiler's
+// wait-count pass cannot tell an LDS read from the direct-to-LDS loads still in flight into the
+// other stages (one dynamic LDS object), so before every such read it can see it drains all of
+// them (vmcnt(0)), which leaves the next tiles' loads half a tile instead of a whole one to land.
+// The kernels' own waits already make each stage's loads land before it is read. A read's
+// result is used only after lds_wait(), whose assembly waits for every LDS read and ties the
+// result registers, so no use can be scheduled before it.
+__device__ __forceinline__ s16x4 lds_read_tr16(const unsigned char* p) {
+  const uint32_t addr =
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)p;
+  s16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+// LEFT: how many of the most recently issued LDS (or scalar) operations may stay outstanding;
+// LDS operations complete in issue order, so every earlier LDS read has returned.
+template <int LEFT = 0, int N>
+__device__ __forceinline__ void lds_wait(s16x4 (&v)[N]) {
+  static_assert(LEFT >= 0 && LEFT <= 15, "lgkmcnt counts up to 15");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(LEFT));
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
 
 // Online-softmax step of one tile for the query row of this lane (the two lane halves hold the
 // same row). Scores arrive raw; masked ones are -inf. The running max m (in units of
@@ -500,30 +523,40 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
 
     // O^T += V^T P^T. For K step (kb, s2) slot e of lane half g2 is key
     // kb*32 + 16*s2 + (e/4)*8 + 4*g2 + e%4 in both operands; the two transpose loads return
-    // slots 0..3 and 4..7 of V^T for column 32*cb + lane % 32.
+    // slots 0..3 and 4..7 of V^T for column 32*cb + lane % 32. All 32 reads of the tile go out
+    // together; the first key block's 16 are waited for before its MFMAs, the rest after them.
+    auto read_v = [&](int step, s16x4 (&vr)[2 * (HD / 32)]) {
+      const int krow = (step >> 1) * 32 + 16 * (step & 1) + 4 * (grp >> 1) + tr_row;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+      for (int cb = 0; cb < HD / 32; ++cb) {
+        const int col = 32 * cb + tr_col;
+        const int chunk = col >> 3, within = (col & 7) * 2;
+        vr[2 * cb] = lds_read_tr16(sv + krow * ROWB + ((chunk ^ key_v(krow)) << 4) + within);
+        vr[2 * cb + 1] =
+            lds_read_tr16(sv + (krow + 8) * ROWB + ((chunk ^ key_v(krow + 8)) << 4) + within);
+      }
+    };
+    s16x4 vbuf[4][2 * (HD / 32)];
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        bf16x8 pf;
+    for (int step = 0; step < 4; ++step) read_v(step, vbuf[step]);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[kb][s2 * 8 + e];
-        const int krow = kb * 32 + 16 * s2 + 4 * (grp >> 1) + tr_row;
+    for (int step = 0; step < 4; ++step) {
+      if (step == 0) {
+        // At most 15 of the 32 still out: the first 16 (key block 0) have returned.
+        lds_wait<15>(vbuf[0]);
+        lds_wait<15>(vbuf[1]);
+      } else if (step == 2) {
+        lds_wait(vbuf[2]);
+        lds_wait(vbuf[3]);
+      }
+      const int kb = step >> 1, s2 = step & 1;
+      bf16x8 pf;
 #pragma unroll
-        for (int cb = 0; cb < HD / 32; ++cb) {
-          const int col = 32 * cb + tr_col;
-          const int chunk = col >> 3, within = (col & 7) * 2;
-          const unsigned char* p0 = sv + krow * ROWB + ((chunk ^ key_v(krow)) << 4) + within;
-          const unsigned char* p1 =
-              sv + (krow + 8) * ROWB + ((chunk ^ key_v(krow + 8)) << 4) + within;
-          const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p0);
-          const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p1);
-          const s16x4 vv[2] = {v0, v1};
-          bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
-          mfma_k16(oacc[cb], vf, pf);
-        }
+      for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[kb][s2 * 8 + e];
+#pragma unroll
+      for (int cb = 0; cb < HD / 32; ++cb) {
+        const s16x4 vv[2] = {vbuf[step][2 * cb], vbuf[step][2 * cb + 1]};
+        mfma_k16(oacc[cb], __builtin_bit_cast(bf16x8, vv), pf);
       }
     }
 
@@ -669,6 +702,25 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
     const bool vis = t < tv;
     const int key0 = (vis ? t : t - tv) * KT;
 
+    // V^T fragments of both K steps, read now so that they land during the scores and softmax
+    // (one wave per SIMD: registers are plentiful). Slot e of lane half g2 in K step s2 is key
+    // 16*s2 + (e/4)*8 + 4*g2 + e%4 in both operands; the two transpose loads return slots 0..3
+    // and 4..7 of V^T for column 32*cb + lane % 32.
+    s16x4 vr[2][2 * (HD / 32)];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int krow = 16 * s2 + 4 * (grp >> 1) + tr_row;
+#pragma unroll
+      for (int cb = 0; cb < HD / 32; ++cb) {
+        const int col = 32 * cb + tr_col;
+        const int chunk = col >> 3, within = (col & 7) * 2;
+        vr[s2][2 * cb] =
+            lds_read_tr16(sv + krow * ROWB + ((chunk ^ stream::key_v(krow)) << 4) + within);
+        vr[s2][2 * cb + 1] = lds_read_tr16(
+            sv + (krow + 8) * ROWB + ((chunk ^ stream::key_v(krow + 8)) << 4) + within);
+      }
+    }
+
     f32x16 sacc = f32x16{};
     {
       const int row = lane & 31;
@@ -694,24 +746,16 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
     online_softmax<16, HD / 32>(scs, a.scale_log2, m_run, l_run, oacc);
 #pragma unroll
     for (int i = 0; i < 16; ++i) sacc[i] = scs[i];
+    lds_wait(vr[0]);
+    lds_wait(vr[1]);
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       bf16x8 pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[s2 * 8 + e];
-      const int krow = 16 * s2 + 4 * (grp >> 1) + tr_row;
 #pragma unroll
       for (int cb = 0; cb < HD / 32; ++cb) {
-        const int col = 32 * cb + tr_col;
-        const int chunk = col >> 3, within = (col & 7) * 2;
-        const unsigned char* p0 = sv + krow * ROWB + ((chunk ^ stream::key_v(krow)) << 4) + within;
-        const unsigned char* p1 =
-            sv + (krow + 8) * ROWB + ((chunk ^ stream::key_v(krow + 8)) << 4) + within;
-        const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p0);
-        const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_s16x4*)(__attribute__((address_space(3))) unsigned char*)p1);
-        const s16x4 vv[2] = {v0, v1};
+        const s16x4 vv[2] = {vr[s2][2 * cb], vr[s2][2 * cb + 1]};
         mfma_k16(oacc[cb], __builtin_bit_cast(bf16x8, vv), pf);
       }
     }
