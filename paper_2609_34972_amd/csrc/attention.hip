@@ -309,12 +309,29 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 // The kernels' own waits already make each stage's loads land before it is read. A read's
 // result is used only after lds_wait(), whose assembly waits for every LDS read and ties the
 // result registers, so no use can be scheduled before it.
-__device__ __forceinline__ s16x4 lds_read_tr16(const unsigned char* p) {
-  const uint32_t addr =
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)p;
+// The LDS address is a per-lane base plus the constant OFF (the instruction's offset field).
+template <int OFF>
+__device__ __forceinline__ s16x4 lds_read_tr16(uint32_t base) {
+  static_assert(OFF >= 0 && OFF < 65536, "16-bit LDS offset");
   s16x4 r;
-  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(addr));
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(base), "n"(OFF));
   return r;
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// V^T fragments of one 16-key step (keys KEY0 .. KEY0 + 15 of the stage's tile) for the four
+// 32-column blocks: col[cb] is the lane's address of key row vrow (< 8) of column block cb
+// relative to the stage (rows 8 apart share the chunk swizzle, so every read of a lane differs
+// only by a constant); the two reads per block return slots 0..3 and 4..7.
+template <int ROWB, int KEY0>
+__device__ __forceinline__ void read_v_step(uint32_t stage, const uint32_t (&col)[4],
+                                            s16x4 (&vr)[8]) {
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb) {
+    vr[2 * cb] = lds_read_tr16<KEY0 * ROWB>(stage + col[cb]);
+    vr[2 * cb + 1] = lds_read_tr16<(KEY0 + 8) * ROWB>(stage + col[cb]);
+  }
 }
 // LEFT: how many of the most recently issued LDS (or scalar) operations may stay outstanding;
 // LDS operations complete in issue order, so every earlier LDS read has returned.
@@ -327,10 +344,11 @@ __device__ __forceinline__ void lds_wait(s16x4 (&v)[N]) {
 }
 
 // Online-softmax step of one tile for the query row of this lane (the two lane halves hold the
-// same row). Scores arrive raw; masked ones are -inf. The running max m (in units of
-// scale*log2 e) is only raised when some row of the wave grew by more than 2^8: between raises
-// p = 2^(s*scale - m) stays below 256, and since the sum and O use the same stale m the result
-// is unchanged while most tiles skip the rescale of O.
+// same row). Scores arrive raw; masked ones are -inf; they leave as p = 2^(s*scale - m). The
+// running max m (in units of scale*log2 e) is only raised when some row of the wave grew by more
+// than 2^8: between raises p stays below 256, and since the sum and O use the same stale m the
+// result is unchanged while most tiles skip the rescale of O. The caller adds the tile's p to
+// the row sum l_run (after rounding them for the P V product, see add_probs).
 template <int NI, int NCB>
 __device__ __forceinline__ void online_softmax(float (&sv)[NI], float scale_log2, float& m_run,
                                                float& l_run, f32x16 (&oacc)[NCB]) {
@@ -348,14 +366,19 @@ __device__ __forceinline__ void online_softmax(float (&sv)[NI], float scale_log2
     for (int cb = 0; cb < NCB; ++cb) oacc[cb] *= alpha;
   }
   const float neg_m = -m_run;
-  float psum = 0.f;
 #pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    const float p = __builtin_amdgcn_exp2f(fmaf(sv[i], scale_log2, neg_m));
-    sv[i] = p;
-    psum += p;
-  }
-  l_run += psum;
+  for (int i = 0; i < NI; ++i) sv[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], scale_log2, neg_m));
+}
+
+// Adds the eight bf16 probabilities of a P fragment to a row sum: the sum is taken over the
+// same rounded values that the P V product multiplies, two per dot-product instruction.
+__device__ __forceinline__ float add_probs(const bf16x8& p, float sum) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    sum = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p[2 * q], p[2 * q + 1]}, one, sum, false);
+  return sum;
 }
 
 // Block-uniform integer that the compiler computes on the vector unit (integer divisions):
@@ -479,6 +502,16 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
   const int l16 = lane & 15, grp = lane >> 4;
   const int tr_row = l16 >> 2;
   const int tr_col = 16 * (grp & 1) + 4 * (l16 & 3);  // plus 32 * cb
+  // V read addresses inside a stage's V tile: key row vrow of the step, column block cb.
+  uint32_t vcol[4];
+  {
+    const int vrow = 4 * (grp >> 1) + tr_row;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int col = 32 * cb + tr_col;
+      vcol[cb] = vrow * ROWB + (((col >> 3) ^ key_v(vrow)) << 4) + (col & 7) * 2;
+    }
+  }
 
   int stage = 0;
   for (int t = t_begin; t < t_end; ++t) {
@@ -525,20 +558,13 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
     // kb*32 + 16*s2 + (e/4)*8 + 4*g2 + e%4 in both operands; the two transpose loads return
     // slots 0..3 and 4..7 of V^T for column 32*cb + lane % 32. All 32 reads of the tile go out
     // together; the first key block's 16 are waited for before its MFMAs, the rest after them.
-    auto read_v = [&](int step, s16x4 (&vr)[2 * (HD / 32)]) {
-      const int krow = (step >> 1) * 32 + 16 * (step & 1) + 4 * (grp >> 1) + tr_row;
-#pragma unroll
-      for (int cb = 0; cb < HD / 32; ++cb) {
-        const int col = 32 * cb + tr_col;
-        const int chunk = col >> 3, within = (col & 7) * 2;
-        vr[2 * cb] = lds_read_tr16(sv + krow * ROWB + ((chunk ^ key_v(krow)) << 4) + within);
-        vr[2 * cb + 1] =
-            lds_read_tr16(sv + (krow + 8) * ROWB + ((chunk ^ key_v(krow + 8)) << 4) + within);
-      }
-    };
     s16x4 vbuf[4][2 * (HD / 32)];
-#pragma unroll
-    for (int step = 0; step < 4; ++step) read_v(step, vbuf[step]);
+    float lsum[2] = {0.f, 0.f};  // two chains of the tile's row sum
+    const uint32_t vs = lds_addr(sv);
+    read_v_step<ROWB, 0>(vs, vcol, vbuf[0]);
+    read_v_step<ROWB, 16>(vs, vcol, vbuf[1]);
+    read_v_step<ROWB, 32>(vs, vcol, vbuf[2]);
+    read_v_step<ROWB, 48>(vs, vcol, vbuf[3]);
 #pragma unroll
     for (int step = 0; step < 4; ++step) {
       if (step == 0) {
@@ -553,12 +579,14 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
       bf16x8 pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[kb][s2 * 8 + e];
+      lsum[s2] = add_probs(pf, lsum[s2]);
 #pragma unroll
       for (int cb = 0; cb < HD / 32; ++cb) {
         const s16x4 vv[2] = {vbuf[step][2 * cb], vbuf[step][2 * cb + 1]};
         mfma_k16(oacc[cb], __builtin_bit_cast(bf16x8, vv), pf);
       }
     }
+    l_run += lsum[0] + lsum[1];
 
     // Tile t+1 has landed (tiles t+2 .. t+NS-1 may still load) and every wave is done with
     // this stage: refill it with tile t+NS.
@@ -687,6 +715,15 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
   const int l16 = lane & 15, grp = lane >> 4;
   const int tr_row = l16 >> 2;
   const int tr_col = 16 * (grp & 1) + 4 * (l16 & 3);
+  uint32_t vcol[4];  // as in k_attn_stream
+  {
+    const int vrow = 4 * (grp >> 1) + tr_row;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int col = 32 * cb + tr_col;
+      vcol[cb] = vrow * ROWB + (((col >> 3) ^ stream::key_v(vrow)) << 4) + (col & 7) * 2;
+    }
+  }
 
   // My tiles: t_begin + wave, + NWAVE, ...  Only this wave reads its stages: waits only.
   int t = t_begin + wave;
@@ -707,19 +744,9 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
     // 16*s2 + (e/4)*8 + 4*g2 + e%4 in both operands; the two transpose loads return slots 0..3
     // and 4..7 of V^T for column 32*cb + lane % 32.
     s16x4 vr[2][2 * (HD / 32)];
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      const int krow = 16 * s2 + 4 * (grp >> 1) + tr_row;
-#pragma unroll
-      for (int cb = 0; cb < HD / 32; ++cb) {
-        const int col = 32 * cb + tr_col;
-        const int chunk = col >> 3, within = (col & 7) * 2;
-        vr[s2][2 * cb] =
-            lds_read_tr16(sv + krow * ROWB + ((chunk ^ stream::key_v(krow)) << 4) + within);
-        vr[s2][2 * cb + 1] = lds_read_tr16(
-            sv + (krow + 8) * ROWB + ((chunk ^ stream::key_v(krow + 8)) << 4) + within);
-      }
-    }
+    const uint32_t vs = lds_addr(sv);
+    read_v_step<ROWB, 0>(vs, vcol, vr[0]);
+    read_v_step<ROWB, 16>(vs, vcol, vr[1]);
 
     f32x16 sacc = f32x16{};
     {
@@ -748,17 +775,20 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
     for (int i = 0; i < 16; ++i) sacc[i] = scs[i];
     lds_wait(vr[0]);
     lds_wait(vr[1]);
+    float lsum[2] = {0.f, 0.f};
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       bf16x8 pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[s2 * 8 + e];
+      lsum[s2] = add_probs(pf, lsum[s2]);
 #pragma unroll
       for (int cb = 0; cb < HD / 32; ++cb) {
         const s16x4 vv[2] = {vr[s2][2 * cb], vr[s2][2 * cb + 1]};
         mfma_k16(oacc[cb], __builtin_bit_cast(bf16x8, vv), pf);
       }
     }
+    l_run += lsum[0] + lsum[1];
     // This stage is consumed (lgkmcnt drained) before it is refilled with tile t + 2*NWAVE.
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));
     asm volatile("" ::: "memory");
