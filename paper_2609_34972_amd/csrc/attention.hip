@@ -539,14 +539,14 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
 #pragma unroll
       for (int i = 0; i < 16; ++i) scs[kb * 16 + i] = sacc[kb][i];
     if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask
+      // The last key of this tile's kind the lane's row sees, relative to the tile: one compare
+      // and select per score.
+      const int last = (vis ? a.Nv - 1 : min(my_text_last, text_lim - 1)) - key0;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = key0 + kb * 32 + acc_row(lane, i);
-          const bool ok = vis ? key < a.Nv : (key <= my_text_last && key < text_lim);
-          if (!ok) scs[kb * 16 + i] = -INFINITY;
-        }
+        for (int i = 0; i < 16; ++i)
+          scs[kb * 16 + i] = kb * 32 + acc_row(lane, i) > last ? -INFINITY : scs[kb * 16 + i];
     }
     online_softmax<32, HD / 32>(scs, a.scale_log2, m_run, l_run, oacc);
 #pragma unroll
@@ -762,13 +762,10 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
     float scs[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) scs[i] = sacc[i];
-    if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask
+    if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask (as above)
+      const int last = (vis ? a.Nv - 1 : min(my_text_last, text_lim - 1)) - key0;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = key0 + acc_row(lane, i);
-        const bool ok = vis ? key < a.Nv : (key <= my_text_last && key < text_lim);
-        if (!ok) scs[i] = -INFINITY;
-      }
+      for (int i = 0; i < 16; ++i) scs[i] = acc_row(lane, i) > last ? -INFINITY : scs[i];
     }
     online_softmax<16, HD / 32>(scs, a.scale_log2, m_run, l_run, oacc);
 #pragma unroll
