@@ -294,10 +294,13 @@ template <int NW> constexpr int blocks_per_cu() { return (160 * 1024) / (stages<
 template <int NW> constexpr int lds_bytes() { return stages<NW>() * STAGE_BYTES; }
 constexpr int BLOCKS_PER_TILE = KT / 4;   // 1 KiB (4-row) load instructions per tensor
 // XOR keys of the 16-byte chunks of a 256-byte LDS row. K rows are read whole-chunk by 16 rows
-// at once (key = row mod 16); V rows are read by the transpose loads as 4 rows x 2 chunks per
-// 16 lanes (key = 2 * (row mod 8) keeps those 8 chunks in distinct bank groups).
+// at once (key = row mod 16). V rows are read by the transpose loads, whose 32-lane halves each
+// take 4 consecutive rows x 4 consecutive chunks (two column blocks of 16 lanes): key =
+// 4 * (row mod 4) gives each of the 4 rows its own quarter of the 64 banks. (A key of
+// 2 * (row mod 8), which separates the 16 lanes of one column block only, measured about one
+// conflict cycle per LDS instruction; this key measures none.)
 __device__ __forceinline__ int key_k(int row) { return row & 15; }
-__device__ __forceinline__ int key_v(int row) { return (row & 7) << 1; }
+__device__ __forceinline__ int key_v(int row) { return (row & 3) << 2; }
 }  // namespace stream
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -322,8 +325,8 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 }
 // V^T fragments of one 16-key step (keys KEY0 .. KEY0 + 15 of the stage's tile) for the four
 // 32-column blocks: col[cb] is the lane's address of key row vrow (< 8) of column block cb
-// relative to the stage (rows 8 apart share the chunk swizzle, so every read of a lane differs
-// only by a constant); the two reads per block return slots 0..3 and 4..7.
+// relative to the stage (rows a multiple of 4 apart share the chunk swizzle, so every read of a
+// lane differs only by a constant); the two reads per block return slots 0..3 and 4..7.
 template <int ROWB, int KEY0>
 __device__ __forceinline__ void read_v_step(uint32_t stage, const uint32_t (&col)[4],
                                             s16x4 (&vr)[8]) {
