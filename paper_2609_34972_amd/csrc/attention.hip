@@ -34,6 +34,10 @@ namespace dv {
 constexpr float NEG_BIG = -1e30f;  // finite start value of the running max
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
+// Non-temporal 16-byte load, for data read once.
+__device__ __forceinline__ u32x4 ld16_stream(const void* p) {
+  return __builtin_nontemporal_load((const u32x4*)p);
+}
 
 template <typename T, int HD, int NW>
 struct AttnCfg {
@@ -292,6 +296,12 @@ template <int NW> constexpr int stages() { return NW == 4 ? 2 : 3; }
 // Streaming blocks that fit in one CU's 160 KiB of LDS.
 template <int NW> constexpr int blocks_per_cu() { return (160 * 1024) / (stages<NW>() * 2 * 64 * 256); }
 template <int NW> constexpr int lds_bytes() { return stages<NW>() * STAGE_BYTES; }
+// Cache-policy bits of the tile loads. A K/V tile that only one block reads is loaded
+// non-temporally (LLaVA-NeXT, 128 rows per kv-head: 91.5 -> 81 us per layer); tiles that
+// several row blocks share keep the default policy, so the later readers still find them in
+// the L2 (Qwen2.5-VL video, seven row blocks: non-temporal loads cost about 1.5%).
+constexpr int CPOL_DEFAULT = 0;
+constexpr int CPOL_NT = 2;
 constexpr int BLOCKS_PER_TILE = KT / 4;   // 1 KiB (4-row) load instructions per tensor
 // XOR keys of the 16-byte chunks of a 256-byte LDS row. K rows are read whole-chunk by 16 rows
 // at once (key = row mod 16). V rows are read by the transpose loads, whose 32-lane halves each
@@ -423,7 +433,7 @@ __device__ __forceinline__ void stream_sync(int ahead) {
   else pipe_sync<waitcnt_imm(0, 0)>();
 }
 
-template <int NW>
+template <int NW, int CPOL>
 __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnArgs a, int row_blocks) {
   using namespace stream;
   constexpr int NS = stages<NW>();
@@ -482,9 +492,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
       const int row = blk * 4 + r4;
       const int soff = (key0 + blk * 4) * ROWB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(sk + blk * 1024), 16,
-                                               r4 * ROWB + ((pc ^ key_k(row)) << 4), soff, 0, 0);
+                                               r4 * ROWB + ((pc ^ key_k(row)) << 4), soff, 0, CPOL);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(sv + blk * 1024), 16,
-                                               r4 * ROWB + ((pc ^ key_v(row)) << 4), soff, 0, 0);
+                                               r4 * ROWB + ((pc ^ key_v(row)) << 4), soff, 0, CPOL);
     }
   };
 
@@ -636,7 +646,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
 // For few query rows per (batch, kv-head) (LLaVA: 64) one block of four waves takes 32 rows
 // and every wave streams a quarter of the 32-key tiles through its own two LDS stages, so all
 // four SIMDs of the CU work and no barrier is needed until the waves merge their partial
-// (max, sum, O) through LDS.
+// (max, sum, O) through LDS. At most two blocks read a tile, one right after the other, and
+// the tiles are loaded non-temporally (LLaVA-7B: about 3% faster than the default policy).
 
 namespace ksplit {
 constexpr int HD = 128;
@@ -703,10 +714,10 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
       const int soff = (key0 + blk * 4) * ROWB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(sk + blk * 1024), 16,
                                                r4 * ROWB + ((pc ^ stream::key_k(row)) << 4), soff,
-                                               0, 0);
+                                               0, stream::CPOL_NT);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(sv + blk * 1024), 16,
                                                r4 * ROWB + ((pc ^ stream::key_v(row)) << 4), soff,
-                                               0, 0);
+                                               0, stream::CPOL_NT);
     }
   };
 
@@ -909,7 +920,9 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
   for (int j0 = k_begin + wave * KPW + grp; j0 < k_end; j0 += stride * U) {
     // Rows stay in their storage type until used (bf16: 4 registers per 8 elements): converted on
     // load they took 64 registers, leaving four waves per SIMD instead of five (about 2% on the
-    // B 64 decode shape, bit-identical).
+    // B 64 decode shape, bit-identical). The cache rows are read exactly once, so they are loaded
+    // non-temporally and do not displace reusable lines from the L2 and the MALL (B 64 decode:
+    // 5.70-5.91 -> 6.37 TB/s).
     u32x4 kr[U][sizeof(T) / 2], vr[U][sizeof(T) / 2];
     bool ok[U];
 #pragma unroll
@@ -920,8 +933,8 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnArgs a) {
       const T* vp = j < a.Nv ? Vvb + (int64_t)j * HD : Vtb + (int64_t)(j - a.Nv) * HD;
 #pragma unroll
       for (int q2 = 0; q2 < (int)(sizeof(T) / 2); ++q2) {
-        kr[u][q2] = ok[u] ? ld16(kp + q2 * (8 / (sizeof(T) / 2))) : u32x4{};
-        vr[u][q2] = ok[u] ? ld16(vp + q2 * (8 / (sizeof(T) / 2))) : u32x4{};
+        kr[u][q2] = ok[u] ? ld16_stream(kp + q2 * (8 / (sizeof(T) / 2))) : u32x4{};
+        vr[u][q2] = ok[u] ? ld16_stream(vp + q2 * (8 / (sizeof(T) / 2))) : u32x4{};
       }
     }
     auto unpack = [&](const u32x4 (&r)[sizeof(T) / 2], float (&x)[8]) {
@@ -1163,12 +1176,16 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
       k_attn_decode<T, HD, 8><<<grid, dim3(256), 0, s>>>(a);
   } else if (p.stream) {
     if constexpr (sizeof(T) == 2 && HD == 128) {
+      using stream::CPOL_DEFAULT;
+      using stream::CPOL_NT;
       static bool once = [] {
-        (void)hipFuncSetAttribute((const void*)k_attn_stream<1>,
+        (void)hipFuncSetAttribute((const void*)k_attn_stream<1, CPOL_DEFAULT>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<1>());
-        (void)hipFuncSetAttribute((const void*)k_attn_stream<2>,
+        (void)hipFuncSetAttribute((const void*)k_attn_stream<2, CPOL_DEFAULT>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<2>());
-        (void)hipFuncSetAttribute((const void*)k_attn_stream<4>,
+        (void)hipFuncSetAttribute((const void*)k_attn_stream<4, CPOL_DEFAULT>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<4>());
+        (void)hipFuncSetAttribute((const void*)k_attn_stream<4, CPOL_NT>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<4>());
         return true;
       }();
@@ -1183,11 +1200,13 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
         (void)once_k;
         k_attn_ksplit<<<grid, dim3(ksplit::NWAVE * 64), ksplit::LDS_BYTES, s>>>(a, p.row_blocks);
       } else if (p.nw == 1)
-        k_attn_stream<1><<<grid, dim3(64), stream::lds_bytes<1>(), s>>>(a, p.row_blocks);
+        k_attn_stream<1, CPOL_DEFAULT><<<grid, dim3(64), stream::lds_bytes<1>(), s>>>(a, p.row_blocks);
       else if (p.nw == 2)
-        k_attn_stream<2><<<grid, dim3(128), stream::lds_bytes<2>(), s>>>(a, p.row_blocks);
+        k_attn_stream<2, CPOL_DEFAULT><<<grid, dim3(128), stream::lds_bytes<2>(), s>>>(a, p.row_blocks);
+      else if (p.row_blocks == 1)  // each tile has one reader
+        k_attn_stream<4, CPOL_NT><<<grid, dim3(256), stream::lds_bytes<4>(), s>>>(a, p.row_blocks);
       else
-        k_attn_stream<4><<<grid, dim3(256), stream::lds_bytes<4>(), s>>>(a, p.row_blocks);
+        k_attn_stream<4, CPOL_DEFAULT><<<grid, dim3(256), stream::lds_bytes<4>(), s>>>(a, p.row_blocks);
     } else {
       return hipErrorInvalidValue;  // the planner only picks this kernel for bf16, hd 128
     }
