@@ -80,6 +80,7 @@ LAZY = [
     ("ksplit_mha", 2, 8, 8, 128, 577, 64, 64),
     ("stream_gqa", 1, 28, 4, 128, 1000, 128, 128),
     ("stream_mha_96rows", 2, 6, 2, 128, 700, 32, 32),
+    ("stream_mha_128rows", 2, 8, 8, 128, 700, 128, 128),
 ]
 
 
