@@ -277,45 +277,39 @@ __device__ __forceinline__ void pipe_mainloop(const BufOperand& A, const BufOper
   pipe_sync<waitcnt_imm(0, 0)>();
 }
 
-// Refill loads of tile t of a run stream (K tile t % nk of run t / nk), with the per-load
-// offsets worked out at each call (a run's operands change from run to run).
-// A t at or past nt (the stream's end) issues out-of-range loads of the last run, which fetch
-// nothing and fill the stage with zeros.
-template <class C, class Operands>
-__device__ __forceinline__ void pipe_issue_run(Operands& operands, int t, int nk, int nt,
-                                               bf16* stage, int va0, int va1, int vb0, int vb1) {
-  const bool past = t >= nt;
-  const int tt = past ? nt - 1 : t;
-  const int run = tt / nk;
-  BufOperand A, B;
-  operands(run, A, B);
-  const int kbytes = past ? kPipeOutOfRange : (tt - run * nk) * C::BK * 2;
+// Refill loads of one K tile of a run's operands. The per-load row offsets (and, for B, the
+// buffer of each load) are the same for every run, so they are worked out once per stream.
+template <class C>
+__device__ __forceinline__ void pipe_issue_rsrc(const PipeLoads<C>& p, const BufOperand& A,
+                                                const BufOperand& B, int kbytes, bf16* stage,
+                                                int va0, int va1, int vb0, int vb1) {
   const int wave = wave_index();
 #pragma unroll
   for (int i = 0; i < C::A_INS; ++i) {
     const int blk = wave * C::A_INS + i;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(A.r0, (lds_void*)(stage + blk * 512), 16,
-                                             (blk & 1) ? va1 : va0, blk * 8 * A.ld_bytes + kbytes,
-                                             0, 0);
+                                             (blk & 1) ? va1 : va0, p.sa[i] + kbytes, 0, 0);
   }
   bf16* sb = stage + C::BM * C::BK;
 #pragma unroll
   for (int i = 0; i < C::B_INS; ++i) {
     const int blk = wave * C::B_INS + i;
-    const int row = blk * 8;
-    const bool first = row < B.nsplit;
-    const int soff = (first ? row : row - B.nsplit) * B.ld_bytes + kbytes;
+    const bool first = blk * 8 < B.nsplit;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(first ? B.r0 : B.r1, (lds_void*)(sb + blk * 512), 16,
-                                             (blk & 1) ? vb1 : vb0, soff, 0, 0);
+                                             (blk & 1) ? vb1 : vb0, p.sb[i] + kbytes, 0, 0);
   }
 }
 
 // Several GEMMs of the same K through one pipeline (e.g. one output tile of consecutive layers).
 // Tile t of the stream is K tile t % nk of run t / nk, nk = K / 64. operands(run, A, B) fills a
-// run's operands (every run has the same row pitches); epilogue(run, acc) consumes a finished
-// run while the loads of the next run's first two tiles are in flight, so the pipeline does not
-// drain between runs. The epilogue may use LDS past the two stages (C::LDS_BYTES) but not the
-// stages themselves, since a landed tile may sit there.
+// run's operands (every run has the same row pitches and the same B split row); epilogue(run,
+// acc) consumes a finished run while the loads of the next run's first two tiles are in flight,
+// so the pipeline does not drain between runs. The epilogue may use LDS past the two stages
+// (C::LDS_BYTES) but not the stages themselves, since a landed tile may sit there.
+// The refill side keeps the run and K tile of the next tile to load and the operands of that run,
+// which it rebuilds only when the run changes: a tile's refill then costs a few scalar adds (a
+// division and the operand addresses at every tile put ~55 dependent scalar instructions ahead
+// of each tile's first MFMA).
 template <class C, class Operands, class Epilogue>
 __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands operands,
                                           Epilogue epilogue) {
@@ -325,14 +319,26 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
 #pragma unroll
     for (int b = 0; b < C::FN; ++b) acc[a][b] = f32x4{};
   const int nk = K / C::BK, nt = nruns * nk;
-  BufOperand A, B;
-  operands(0, A, B);
-  const int va0 = pipe_lane_offset(A.ld_bytes, 0), va1 = pipe_lane_offset(A.ld_bytes, 1);
-  const int vb0 = pipe_lane_offset(B.ld_bytes, 0), vb1 = pipe_lane_offset(B.ld_bytes, 1);
+  BufOperand An, Bn;  // operands of the run of the next tile to load
+  operands(0, An, Bn);
+  const int va0 = pipe_lane_offset(An.ld_bytes, 0), va1 = pipe_lane_offset(An.ld_bytes, 1);
+  const int vb0 = pipe_lane_offset(Bn.ld_bytes, 0), vb1 = pipe_lane_offset(Bn.ld_bytes, 1);
+  const PipeLoads<C> pl = pipe_loads<C>(An, Bn);
+  int rn = 0, kn = 0;  // run and K tile of the next tile to load
+  // Issues the next tile (past the stream's end: out-of-range loads of the last run, which fetch
+  // nothing and fill the stage with zeros) and steps to the one after it.
+  auto refill = [&](bf16* stage) {
+    const int kbytes = rn < nruns ? kn * C::BK * 2 : kPipeOutOfRange;
+    pipe_issue_rsrc<C>(pl, An, Bn, kbytes, stage, va0, va1, vb0, vb1);
+    if (++kn == nk) {
+      kn = 0;
+      if (++rn < nruns) operands(rn, An, Bn);
+    }
+  };
 
-  pipe_issue_run<C>(operands, 0, nk, nt, lds, va0, va1, vb0, vb1);
+  refill(lds);
   if (nt > 1) {
-    pipe_issue_run<C>(operands, 1, nk, nt, lds + C::STAGE, va0, va1, vb0, vb1);
+    refill(lds + C::STAGE);
     pipe_sync<waitcnt_imm(C::INS, 0)>();
   } else {
     pipe_sync<waitcnt_imm(0, 0)>();
@@ -350,7 +356,7 @@ __device__ __forceinline__ void pipe_runs(int nruns, int K, bf16* lds, Operands 
 #pragma unroll
       for (int b = 0; b < C::FN; ++b) asm volatile("" : "+v"(acc[a][b]));
     pipe_sync<waitcnt_imm(0, 0)>();
-    pipe_issue_run<C>(operands, t + 2, nk, nt, s, va0, va1, vb0, vb1);
+    refill(s);
     pipe_frags<C>(lds + ((t + 1) & 1) * C::STAGE, 0, fa[0], fb[0]);
     pipe_mfmas<C>(acc, fa[1], fb[1]);
     pipe_step1_pattern<C>();
