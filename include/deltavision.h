@@ -119,6 +119,23 @@ dv_status dv_set_fused_kv(int32_t on);
 int32_t dv_project_visual_kv_fused(int32_t d, int32_t r, int32_t Hkv, int32_t hd, int32_t dtype);
 
 /*
+ * Kernel for M_l * gamma_l and the row sums of squares in the bf16 projection (dv_project_visual_kv,
+ * dv_project_visual_kv_ex, dv_kept_visual_kv); both compute Eq. 5 and the RMSNorm statistics of
+ * Eq. 7 with the same products in the same order, so M_l * gamma_l is the same to the bit and
+ * only the order in which the row sum of squares is added up differs.
+ *   1 (tiled): each block computes a 128 x 128 tile of M_l for up to four layers.
+ *   2 (Z-resident): each block takes 128 rows of one layer, keeps their Z_l in registers and
+ *     walks all of d, streaming only U_l; for r = 256 or 512 (other ranks take the tiled kernel).
+ *   0 (default): the Z-resident kernel where r is 256 and there are at least eight rounds
+ *     (2048) of its blocks (ceil(B*Nv / 128) * nl), else the tiled kernel.
+ * dv_set_up_kernel(mode) selects, process-wide (a call already enqueued keeps its kernel);
+ * mode must be 0, 1 or 2. dv_project_visual_kv_up_kernel returns the kernel (1 or 2) a bf16 call
+ * with these sizes takes under the current setting, 1 for any other dtype; no GPU work.
+ */
+dv_status dv_set_up_kernel(int32_t mode);
+int32_t dv_project_visual_kv_up_kernel(int64_t T, int32_t d, int32_t r, int32_t nl, int32_t dtype);
+
+/*
  * Recurrent adapter (Section 3.1, Eq. 6) and the visual K/V projection (Section 3.2, Eq. 7) of
  * every layer in one call:
  *     M_{-1} = E,   M_l = M_{l-1} + phi(M_{l-1} D_l) U_l,   l = 0 .. L-1,

@@ -13,7 +13,7 @@ from ._lib import (ACT_GELU, ACT_SILU, ATTENTION_SCRATCH_BYTES, KERNEL_ATTENTION
                    DeltaVisionError, KVEpilogue, build_visual_memory, delta_rule_workspace,
                    delta_rule_write, kept_visual_kv,
                    kept_visual_kv_workspace, load, probe_mfma, project_visual_kv,
-                   project_visual_kv_fused, set_fused_kv,
+                   project_visual_kv_fused, set_fused_kv, set_up_kernel, project_visual_kv_up_kernel,
                    project_visual_kv_ex_workspace,
                    project_visual_kv_workspace, recurrent_visual_kv,
                    recurrent_visual_kv_workspace, text_visual_attention,
@@ -21,7 +21,7 @@ from ._lib import (ACT_GELU, ACT_SILU, ATTENTION_SCRATCH_BYTES, KERNEL_ATTENTION
 
 __all__ = [
     "ACT_SILU", "ACT_GELU", "DeltaVisionError", "load", "build_visual_memory",
-    "project_visual_kv", "project_visual_kv_workspace", "project_visual_kv_fused", "set_fused_kv", "project_visual_kv_ex_workspace",
+    "project_visual_kv", "project_visual_kv_workspace", "project_visual_kv_fused", "set_fused_kv", "set_up_kernel", "project_visual_kv_up_kernel", "project_visual_kv_ex_workspace",
     "KVEpilogue", "recurrent_visual_kv",
     "recurrent_visual_kv_workspace", "kept_visual_kv", "kept_visual_kv_workspace",
     "text_visual_attention", "text_visual_attention_noalloc", "ATTENTION_SCRATCH_BYTES",

@@ -28,6 +28,8 @@ EXPORTS = (
     "dv_project_visual_kv",
     "dv_project_visual_kv_fused",
     "dv_set_fused_kv",
+    "dv_set_up_kernel",
+    "dv_project_visual_kv_up_kernel",
     "dv_text_visual_attention_workspace",
     "dv_text_visual_attention",
     "dv_text_visual_attention_noalloc",
@@ -104,6 +106,10 @@ def load() -> ctypes.CDLL:
         lib.dv_project_visual_kv_fused.restype = i32
         lib.dv_set_fused_kv.argtypes = [i32]
         lib.dv_set_fused_kv.restype = i32
+        lib.dv_set_up_kernel.argtypes = [i32]
+        lib.dv_set_up_kernel.restype = i32
+        lib.dv_project_visual_kv_up_kernel.argtypes = [i64, i32, i32, i32, i32]
+        lib.dv_project_visual_kv_up_kernel.restype = i32
         lib.dv_project_visual_kv_ex_workspace.argtypes = [i64, i32, i32, i32, i32]
         lib.dv_project_visual_kv_ex_workspace.restype = sz
         lib.dv_project_visual_kv_ex.argtypes = ([vp] * 8 + [i32] * 9 + [f32, ctypes.POINTER(_KvEpilogue), i32, vp, sz, vp])
@@ -224,6 +230,18 @@ def project_visual_kv_fused(d: int, r: int, Hkv: int, hd: int, dtype: torch.dtyp
     """Whether project_visual_kv (no epilogue) takes the fused up + norm + K/V kernel now."""
     code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
     return bool(load().dv_project_visual_kv_fused(d, r, Hkv, hd, code))
+
+
+def set_up_kernel(mode: int) -> None:
+    """Kernel for M * gamma and the row sums of squares in the bf16 projection: 0 by shape, 1 the
+    tiled kernel, 2 the Z-resident kernel where it applies (process-wide)."""
+    _check(load().dv_set_up_kernel(int(mode)))
+
+
+def project_visual_kv_up_kernel(T: int, d: int, r: int, nl: int, dtype: torch.dtype) -> int:
+    """The kernel (1 tiled, 2 Z-resident) a projection call with these sizes takes now."""
+    code = DV_BF16 if dtype == torch.bfloat16 else DV_F32
+    return int(load().dv_project_visual_kv_up_kernel(int(T), int(d), int(r), int(nl), code))
 
 
 def set_fused_kv(on: bool) -> None:

@@ -179,6 +179,18 @@ dv_status dv_set_fused_kv(int32_t on) {
   return ok();
 }
 
+dv_status dv_set_up_kernel(int32_t mode) {
+  if (mode < 0 || mode > 2) return fail(DV_ERR_SHAPE, "mode must be 0, 1 or 2 (got %d)", mode);
+  dv::set_up_kernel(mode);
+  return ok();
+}
+
+int32_t dv_project_visual_kv_up_kernel(int64_t T, int32_t d, int32_t r, int32_t nl,
+                                       int32_t dtype) {
+  if (T <= 0 || d <= 0 || r <= 0 || nl <= 0 || dtype != DV_BF16) return 1;
+  return dv::up_z_resident(T, d, r, nl) ? 2 : 1;
+}
+
 }  // extern "C"
 
 namespace {

@@ -19,6 +19,9 @@
 #include "gemm_pipe.hpp"
 #include "gemm_tile.hpp"
 
+#include <atomic>
+#include <utility>
+
 namespace dv {
 
 // ---------------------------------------------------------------- tiles
@@ -431,6 +434,289 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
     }
   };
   pipe_runs<C>(nrun, r, (bf16*)smem, operands, epilogue);
+}
+
+// ------------------------------------------------------------------ up projection, Z resident
+//
+// For a large rank (r = 512) and many token tiles the up projection can run the other way
+// round: a block takes one 128-row tile of one layer and walks every 128-column tile of d, and
+// each of its four waves (64 x 64 of the tile, one per SIMD) holds its 64 rows of Z_l for the
+// whole layer in registers (r / 2 of them, mostly accumulation registers, which the MFMAs read
+// directly). Only U streams through LDS, in a four-deep ring per wave that no other wave reads,
+// so the main loop has no barrier, and every wave sees whole rows of M: the block writes the
+// full-row sum of squares (one partial per row instead of one per column tile). E comes through
+// the wave's LDS as whole 128-byte rows and is read back in the accumulator layout; the same
+// buffer then turns M * gamma around for the stores.
+// Every load and store of the loop is a buffer instruction issued unconditionally (rows and
+// columns outside the tensors take out-of-range offsets: loads return zeros, stores are dropped)
+// and the LDS traffic is inline assembly, so the number of memory instructions a wave has in
+// flight is the same on every path and the waits below count them exactly.
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+namespace upz {
+constexpr int BM = 128, BN = 128, NW = 4, WM = 64, WN = 64, FM = WM / 16, FN = WN / 16;
+constexpr int D = 4;                          // U tiles in flight per wave
+constexpr int TILE = WN * 128;                // one wave's U tile: 64 columns x 64 k (8 KiB)
+constexpr int RING = D * TILE;
+constexpr int EBUF = WM * WN * 2;             // one wave's E tile (8 KiB), then the turnaround
+constexpr int SCR_PITCH = WN + 8;             // bf16 per row of the store turnaround
+constexpr int WAVE_LDS = RING + EBUF;
+constexpr int LDS_BYTES = NW * WAVE_LDS;      // 160 KiB; the row-sum exchange reuses it
+constexpr int DMA = TILE / 1024;              // 1 KiB load instructions per U tile
+// Counted loads per column tile: E's. Only instructions the compiler cannot move are counted
+// (loads into LDS and stores have side effects and keep their order); gamma's loads write
+// registers, may be moved (the compiler waits for them itself), and an uncounted instruction only
+// makes a wait stricter.
+constexpr int G = EBUF / 1024;
+constexpr int S = 2 * FM;                     // M * gamma stores per column tile
+constexpr uint32_t OOR = 0x80000000u;         // past every buffer's range
+constexpr int CPOL_NT = 2;                    // non-temporal: M * gamma is read by the next launch
+static_assert(DMA * (D - 1) + S + G <= 63, "vmcnt counts every instruction in flight");
+static_assert(16 * SCR_PITCH * 2 <= EBUF, "the turnaround fits in the E buffer");
+
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "16-bit LDS offset");
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+  return r;
+}
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_b64(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "16-bit LDS offset");
+  u32x2 r;
+  asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+  return r;
+}
+__device__ __forceinline__ void lds_write_b64(uint32_t addr, u32x2 v) {
+  asm volatile("ds_write_b64 %0, %1" ::"v"(addr), "v"(v) : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// Wait for the LDS reads in flight and tie their results to this point.
+template <class V, int N>
+__device__ __forceinline__ void lds_wait(V (&v)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
+// Vector-memory wait for the U tile after tile kt of a column tile. In flight, oldest first:
+// that tile, the D - 1 tiles after it, and, for kt <= D - 2, the previous column tile's stores
+// and this column tile's E loads, issued after that tile's loads.
+template <int KT, bool FIRST>
+__device__ __forceinline__ void wait_next() {
+  constexpr int n = DMA * (D - 1) + (KT <= D - 2 ? G + (FIRST ? 0 : S) : 0);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(n, 15));
+  asm volatile("" ::: "memory");
+}
+}  // namespace upz
+
+template <int R>
+__global__ __launch_bounds__(upz::NW * 64, 1) void k_up_norm_zr(
+    const bf16* __restrict__ E, const bf16* __restrict__ Z, const bf16* __restrict__ Uw,
+    const bf16* __restrict__ gamma, bf16* __restrict__ Mg, float* __restrict__ ssq, int T, int d,
+    int l0, int nl) {
+  using namespace upz;
+  constexpr int KS = R / 32;   // 32-deep MFMA steps per column tile
+  constexpr int NKT = R / 64;  // 64-deep U tiles per column tile
+  static_assert(NKT % D == 0 && NKT >= D, "the ring slot of a tile is its index mod D");
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x & 63, wave = wave_index();
+  const int wm = wave >> 1, wn = wave & 1;
+  // Layer-major block order: the blocks an XCD holds at once share a layer and so its U.
+  const int n_rt = (T + BM - 1) / BM;
+  const int lz = blockIdx.x / n_rt, m0 = (blockIdx.x - lz * n_rt) * BM;
+  const int l = l0 + lz;
+  const int ncol = (d + BN - 1) / BN;
+  const int row0 = m0 + wm * WM + (lane & 15);  // + 16 a: this lane's rows
+  const int kq = 8 * (lane >> 4);                 // this lane's k offset within a 32-deep step
+
+  // Z_l rows of this wave, in the B-operand layout of the MFMAs (swapped, as in the GEMMs).
+  const __amdgpu_buffer_rsrc_t rz = buffer_rsrc(Z + (int64_t)l * T * R, (int64_t)T * R * 2);
+  bf16x8 zf[KS][FM];
+#pragma unroll
+  for (int s = 0; s < KS; ++s)
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+      zf[s][a] = __builtin_bit_cast(
+          bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                      rz, ((row0 + 16 * a) * R + 32 * s + kq) * 2, 0, 0));
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));  // Z is complete before the streams start
+
+  // U tile p of the stream (column tile p / NKT, K tile p % NKT) of this wave: rows
+  // j*128 + wn*64 + 0..63 of U_l (the output columns), bytes 128*kt .. +127 of each row, into
+  // ring slot p % D with the GEMM pipeline's swizzled layout. E tiles use the same layout.
+  const __amdgpu_buffer_rsrc_t ru = buffer_rsrc(Uw + (int64_t)l * d * R, (int64_t)d * R * 2);
+  const __amdgpu_buffer_rsrc_t re = buffer_rsrc(E, (int64_t)T * d * 2);
+  const __amdgpu_buffer_rsrc_t rg = buffer_rsrc(gamma + (int64_t)l * d, (int64_t)d * 2);
+  const __amdgpu_buffer_rsrc_t rm = buffer_rsrc(Mg + (int64_t)lz * T * d, (int64_t)T * d * 2);
+  const int ua0 = pipe_lane_offset(R * 2, 0), ua1 = pipe_lane_offset(R * 2, 1);
+  const int ea0 = pipe_lane_offset(d * 2, 0), ea1 = pipe_lane_offset(d * 2, 1);
+  unsigned char* ring = smem + wave * WAVE_LDS;
+  unsigned char* ebuf = ring + RING;
+  auto issue_u = [&](int j, int kt, int slot) {
+    const bool in = j < ncol;
+    const int sbase = (j * BN + wn * WN) * R * 2 + kt * 128;
+#pragma unroll
+    for (int blk = 0; blk < DMA; ++blk)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ru, (lds_void*)(ring + slot * TILE + blk * 1024), 16, (blk & 1) ? ua1 : ua0,
+          in ? sbase + blk * 8 * R * 2 : (int)OOR, 0, 0);
+  };
+  // E rows m0 + wm*64 + 0..63, columns c0 .. c0 + 63 (128 bytes of each row), and gamma.
+  u32x2 g4[FN];
+  auto issue_eg = [&](int j) {
+    const int c0 = j * BN + wn * WN;
+    const bool in = c0 < d;  // d % 64 == 0: the wave's 64 columns are all in or out
+#pragma unroll
+    for (int blk = 0; blk < EBUF / 1024; ++blk) {
+      const int r8 = m0 + wm * WM + blk * 8;  // rows past T read zeros (past the range)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(re, (lds_void*)(ebuf + blk * 1024), 16,
+                                               (blk & 1) ? ea1 : ea0,
+                                               in ? (r8 * d + c0) * 2 : (int)OOR, 0, 0);
+    }
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
+      g4[b] = __builtin_amdgcn_raw_buffer_load_b64(
+          rg, in ? (c0 + 16 * b + 4 * (lane >> 4)) * 2 : OOR, 0, 0);
+  };
+  // Fragment b of K step s2 of a U tile: row b*16 + lane%16, 16-byte chunk 4*s2 + lane/16, XOR
+  // key (row / 2) % 8 = (lane % 16) / 2. E in the accumulator layout: row a*16 + lane%16, bytes
+  // 8*(lane/16) + 32 b of the row, i.e. chunk 2b + lane/32 at byte 8*((lane/16) % 2).
+  const uint32_t ring_addr = lds_addr(ring), e_addr = lds_addr(ebuf);
+  const int key = (lane & 15) >> 1;
+  uint32_t fo[2];
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2)
+    fo[s2] = ring_addr + (lane & 15) * 128 + (((4 * s2 + (lane >> 4)) ^ key) << 4);
+  uint32_t eo[FN];
+#pragma unroll
+  for (int b = 0; b < FN; ++b)
+    eo[b] = e_addr + (lane & 15) * 128 + (((2 * b + (lane >> 5)) ^ key) << 4) + 8 * ((lane >> 4) & 1);
+  const uint32_t scr_w = e_addr + ((lane & 15) * SCR_PITCH + 4 * (lane >> 4)) * 2;
+  const uint32_t scr_r = e_addr + ((lane >> 3) * SCR_PITCH + (lane & 7) * 8) * 2;
+
+  auto read_frags = [&](auto slotc, u32x4 (&f)[2][FN]) {
+    constexpr int slot = decltype(slotc)::value;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      f[s2][0] = upz::lds_read_b128<slot * TILE + 0 * 2048>(fo[s2]);
+      f[s2][1] = upz::lds_read_b128<slot * TILE + 1 * 2048>(fo[s2]);
+      f[s2][2] = upz::lds_read_b128<slot * TILE + 2 * 2048>(fo[s2]);
+      f[s2][3] = upz::lds_read_b128<slot * TILE + 3 * 2048>(fo[s2]);
+    }
+  };
+
+#pragma unroll
+  for (int kt = 0; kt < D; ++kt) issue_u(0, kt, kt);
+  issue_eg(0);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(DMA * (D - 1) + G, 15));  // U tile 0 landed
+  asm volatile("" ::: "memory");
+  u32x4 fr[2][2][FN];  // fragments of the current and the next U tile
+  read_frags(std::integral_constant<int, 0>{}, fr[0]);
+  float ss[FM] = {0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < ncol; ++j) {
+    const int c0 = j * BN + wn * WN;  // this wave's first column
+    const bool cols_ok = c0 < d;
+    if (j > 0) issue_eg(j);
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+      for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{};
+    const bool first = j == 0;
+    static_for<0, NKT>([&](auto ktc) {
+      constexpr int kt = decltype(ktc)::value, slot = kt % D, cur = kt & 1;
+      upz::lds_wait(fr[cur][0]);
+      upz::lds_wait(fr[cur][1]);
+      // This tile's slot is read: refill it with the tile D ahead in the stream.
+      constexpr int nxt = kt + D;
+      issue_u(nxt < NKT ? j : j + 1, nxt % NKT, slot);
+      // The next tile (the next column tile's first one after the last) lands, then its
+      // fragments are read while this tile's MFMAs run.
+      if (first) upz::wait_next<kt, true>();
+      else upz::wait_next<kt, false>();
+      read_frags(std::integral_constant<int, (kt + 1) % D>{}, fr[cur ^ 1]);
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+          for (int b = 0; b < FN; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, fr[cur][s2][b]), zf[2 * kt + s2][a], acc[a][b], 0, 0,
+                0);
+    });
+    static_assert(NKT % 2 == 0, "the next column tile's first fragments sit in fr[0]");
+
+    // Epilogue: M = acc + E, the row sums of squares of fp32 M, M * gamma rounded to bf16 and
+    // turned around through the E buffer so that every store writes 16-byte pieces of rows.
+    // E of this column tile landed before the last wait above (it was issued before the U tile
+    // waited for there).
+#pragma unroll
+    for (int a = 0; a < FM; ++a) {
+      u32x2 e4[FN];
+      e4[0] = upz::lds_read_b64<0>(eo[0] + a * 16 * 128);
+      e4[1] = upz::lds_read_b64<0>(eo[1] + a * 16 * 128);
+      e4[2] = upz::lds_read_b64<0>(eo[2] + a * 16 * 128);
+      e4[3] = upz::lds_read_b64<0>(eo[3] + a * 16 * 128);
+      upz::lds_wait(e4);
+      ss[a] += 0.f;
+#pragma unroll
+      for (int b = 0; b < FN; ++b) {
+        const bf16x4 e = __builtin_bit_cast(bf16x4, e4[b]);
+        const bf16x4 g = __builtin_bit_cast(bf16x4, g4[b]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float m = acc[a][b][u] + (float)e[u];
+          ss[a] += m * m;
+          acc[a][b][u] = m * (float)g[u];
+        }
+      }
+    }
+#pragma unroll
+    for (int a = 0; a < FM; ++a) {
+#pragma unroll
+      for (int b = 0; b < FN; ++b) {
+        bf16x4 o;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) o[u] = (bf16)acc[a][b][u];
+        upz::lds_write_b64(scr_w + b * 32, __builtin_bit_cast(u32x2, o));
+      }
+      u32x4 v[2];
+      v[0] = upz::lds_read_b128<0>(scr_r);
+      v[1] = upz::lds_read_b128<8 * SCR_PITCH * 2>(scr_r);
+      upz::lds_wait(v);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int row = m0 + wm * WM + a * 16 + h * 8 + (lane >> 3);
+        __builtin_amdgcn_raw_buffer_store_b128(
+            v[h], rm, (cols_ok && row < T) ? (row * d + c0 + (lane & 7) * 8) * 2 : OOR, 0,
+            CPOL_NT);
+      }
+    }
+  }
+  // Row sums of squares: the four lanes of a row, then the two column halves through LDS.
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));  // nothing of the streams is in flight
+  __syncthreads();
+  float* ssx = (float*)smem;
+#pragma unroll
+  for (int a = 0; a < FM; ++a) {
+    float s = ss[a];
+    s += shfl_xor(s, 16);
+    s += shfl_xor(s, 32);
+    if (lane < 16) ssx[wn * BM + wm * WM + a * 16 + lane] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x < BM && m0 + (int)threadIdx.x < T)
+    ssq[(int64_t)lz * T + m0 + threadIdx.x] = ssx[threadIdx.x] + ssx[BM + threadIdx.x];
 }
 
 // Backbone epilogue arguments as the kernels see them (see KvEpiArgs).
@@ -892,6 +1178,24 @@ hipError_t launch_kv_only(const void* Mg, const float* ssq, const void* Wk, cons
   return hipGetLastError();
 }
 
+static std::atomic<int> g_up_kernel{0};
+void set_up_kernel(int mode) { g_up_kernel.store(mode, std::memory_order_relaxed); }
+
+bool up_z_resident(int64_t T, int d, int r, int nl) {
+  const int mode = g_up_kernel.load(std::memory_order_relaxed);
+  if (mode == 1 || (r != 256 && r != 512)) return false;
+  // 32-bit buffer offsets: E, M * gamma and Z_l within 2^31 bytes, U_l below the out-of-range
+  // offset of the tile stream.
+  if (T * d * 2 >= (int64_t(1) << 31) || T * r * 2 >= (int64_t(1) << 31) ||
+      (int64_t)d * r * 2 >= (int64_t(1) << 30))
+    return false;
+  if (mode == 2) return true;
+  // By shape: r = 256 with at least eight rounds of 256 blocks (LLaVA-NeXT: 2.88 -> 2.73 ms).
+  // At r = 512 the tiled kernel is faster (Qwen2.5-VL video 2.24 against 2.34 ms), and a few
+  // rounds leave too large a tail for blocks that each walk all of d.
+  return r == 256 && (int64_t)cdiv(T, upz::BM) * nl >= 8 * 256;
+}
+
 static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, const void* gamma,
                                  const void* Wk, const void* Wv, void* Kv, void* Vv, int B_,
                                  int Nv, int d, int r, int Hkv, int hd, int l0, int nl, float eps,
@@ -903,6 +1207,8 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
     allow_lds(k_kv_proj_p<false>, kv_lds);
     allow_lds(k_kv_proj_p<true>, kv_lds);
     allow_lds(k_up_norm_p<UpP>, UpLds<UpP>::BYTES);
+    allow_lds(k_up_norm_zr<256>, upz::LDS_BYTES);
+    allow_lds(k_up_norm_zr<512>, upz::LDS_BYTES);
     return true;
   }();
   (void)once;
@@ -915,13 +1221,26 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
     return e;
   }
   const int T_ = B_ * Nv;
-  const int np = cdiv(d, UpP::BN);
-  dim3 gu(np, cdiv(T_, UpP::BM), cdiv(nl, kUpLayers));
-  const TileOrder uo = up_order();
+  const bool zres = up_z_resident(T_, d, r, nl);
+  const int np = zres ? 1 : cdiv(d, UpP::BN);  // sums of squares per row
   if (first) record(ev.up[0], s);
-  k_up_norm_p<UpP><<<gu, dim3(UpP::NT), UpLds<UpP>::BYTES, s>>>(
-      (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_, d, r,
-      l0, nl, uo.sh, uo.sw);
+  if (zres) {
+    const dim3 gz((unsigned)(cdiv(T_, upz::BM) * nl));
+    if (r == 512)
+      k_up_norm_zr<512><<<gz, dim3(upz::NW * 64), upz::LDS_BYTES, s>>>(
+          (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_,
+          d, l0, nl);
+    else
+      k_up_norm_zr<256><<<gz, dim3(upz::NW * 64), upz::LDS_BYTES, s>>>(
+          (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_,
+          d, l0, nl);
+  } else {
+    dim3 gu(np, cdiv(T_, UpP::BM), cdiv(nl, kUpLayers));
+    const TileOrder uo = up_order();
+    k_up_norm_p<UpP><<<gu, dim3(UpP::NT), UpLds<UpP>::BYTES, s>>>(
+        (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_,
+        d, r, l0, nl, uo.sh, uo.sw);
+  }
   if (last) record(ev.up[1], s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

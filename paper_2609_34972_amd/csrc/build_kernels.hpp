@@ -59,6 +59,12 @@ hipError_t launch_project_kv(const void* E, const void* Z, const void* Uw, const
                              void* Mg, float* ssq, hipStream_t s, const LaunchEvents& ev,
                              bool first_group, bool last_group, const KvEpiArgs* epi = nullptr);
 
+// Which kernel computes M_l * gamma_l and the row sums of squares for the bf16 projection:
+// 0 picks by shape (the Z-resident kernel for r = 256 once there are at least eight rounds of its
+// blocks), 1 always the tiled kernel, 2 the Z-resident kernel wherever it applies (r = 256, 512).
+void set_up_kernel(int mode);
+bool up_z_resident(int64_t T, int d, int r, int nl);
+
 // The fused kernel (fused_kv.hip) computes M_l, its RMSNorm and the K/V projection of 64 tokens
 // in one block and needs no workspace. It covers bf16, 2 Hkv hd = 1024, r in {128, 256, 512},
 // d a multiple of 64, no backbone epilogue (up_kv_fused_eligible), and the projection takes it

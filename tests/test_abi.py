@@ -132,6 +132,32 @@ def test_project_visual_kv_fused_rule(lib):
     assert all(lib.dv_project_visual_kv_fused(*a) == 0 for a in eligible)
 
 
+def test_up_kernel_rule(lib):
+    """By shape the Z-resident up kernel takes r = 256 with at least 2048 blocks (128-row tiles
+    times layers); forced (mode 2) it takes r = 256 or 512; mode 1 always the tiled kernel."""
+    next_shape = (8 * 2880, 4096, 256, 32, BF16)     # LLaVA-NeXT: 180 x 32 blocks
+    llava = (4 * 576, 4096, 256, 32, BF16)           # LLaVA-7B: 18 x 32 blocks
+    qwen = (16384, 3584, 512, 28, BF16)               # Qwen2.5-VL video: r = 512
+    others = [(16384, 3584, 128, 28, BF16),           # rank 128
+              (16384, 3584, 256, 28, F32),            # fp32
+              (1 << 21, 4096, 256, 32, BF16),         # E beyond 2^31 bytes
+              (0, 4096, 256, 32, BF16)]
+    assert lib.dv_project_visual_kv_up_kernel(*next_shape) == 2
+    assert lib.dv_project_visual_kv_up_kernel(*llava) == 1
+    assert lib.dv_project_visual_kv_up_kernel(*qwen) == 1
+    assert all(lib.dv_project_visual_kv_up_kernel(*a) == 1 for a in others)
+    assert lib.dv_set_up_kernel(3) == SHAPE and lib.dv_set_up_kernel(-1) == SHAPE
+    try:
+        assert lib.dv_set_up_kernel(2) == 0
+        assert all(lib.dv_project_visual_kv_up_kernel(*a) == 2 for a in (next_shape, llava, qwen))
+        assert all(lib.dv_project_visual_kv_up_kernel(*a) == 1 for a in others)
+        assert lib.dv_set_up_kernel(1) == 0
+        assert all(lib.dv_project_visual_kv_up_kernel(*a) == 1 for a in (next_shape, llava, qwen))
+    finally:
+        assert lib.dv_set_up_kernel(0) == 0
+    assert lib.dv_project_visual_kv_up_kernel(*next_shape) == 2
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(Q=None), NULL), (dict(Kt=None), NULL), (dict(O=None), NULL), (dict(Kv=None), NULL),
     (dict(Vt=FAKE + 4), ALIGN),
