@@ -668,7 +668,6 @@ __global__ __launch_bounds__(upz::NW * 64, 1) void k_up_norm_zr(
       e4[2] = upz::lds_read_b64<0>(eo[2] + a * 16 * 128);
       e4[3] = upz::lds_read_b64<0>(eo[3] + a * 16 * 128);
       upz::lds_wait(e4);
-      ss[a] += 0.f;
 #pragma unroll
       for (int b = 0; b < FN; ++b) {
         const bf16x4 e = __builtin_bit_cast(bf16x4, e4[b]);
