@@ -1179,8 +1179,6 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
       using stream::CPOL_DEFAULT;
       using stream::CPOL_NT;
       static bool once = [] {
-        (void)hipFuncSetAttribute((const void*)k_attn_stream<1, CPOL_DEFAULT>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<1>());
         (void)hipFuncSetAttribute((const void*)k_attn_stream<2, CPOL_DEFAULT>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<2>());
         (void)hipFuncSetAttribute((const void*)k_attn_stream<4, CPOL_DEFAULT>,
@@ -1199,9 +1197,7 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
         }();
         (void)once_k;
         k_attn_ksplit<<<grid, dim3(ksplit::NWAVE * 64), ksplit::LDS_BYTES, s>>>(a, p.row_blocks);
-      } else if (p.nw == 1)
-        k_attn_stream<1, CPOL_DEFAULT><<<grid, dim3(64), stream::lds_bytes<1>(), s>>>(a, p.row_blocks);
-      else if (p.nw == 2)
+      } else if (p.nw == 2)  // the planner gives the streaming kernel two or four waves
         k_attn_stream<2, CPOL_DEFAULT><<<grid, dim3(128), stream::lds_bytes<2>(), s>>>(a, p.row_blocks);
       else if (p.row_blocks == 1)  // each tile has one reader
         k_attn_stream<4, CPOL_NT><<<grid, dim3(256), stream::lds_bytes<4>(), s>>>(a, p.row_blocks);
