@@ -59,6 +59,12 @@ BUILD = [
     # fp32 engine
     configs.TINY.with_(name="g_f32", d=320, L=3, r=48, Hq=6, Hkv=3, hd=128, B=2, Nv=35,
                        act=configs.ACT_SILU),
+    # the Z-resident up projection (forced): ragged rows, a half column tile (d = 960), r = 256
+    # and r = 512
+    configs.LLAVA7B.with_(name="g_zr_r256", d=960, L=2, r=256, Hq=4, Hkv=2, hd=128, B=1, Nv=100,
+                          outlier_channels=(211, 723)),
+    configs.QWEN25VL_VIDEO.with_(name="g_zr_r512", d=1024, L=2, r=512, Hq=8, Hkv=4, hd=64, B=3,
+                                 Nv=37, Nt=16),
 ]
 
 
@@ -67,10 +73,14 @@ def test_build_and_projection_stay_inside(w):
     say(f"[guard build {w.name}]")
     fused = w.name.startswith("g_fused")
     dvl.set_fused_kv(fused)
+    dvl.set_up_kernel(2 if w.name.startswith("g_zr") else 0)
     try:
+        if w.name.startswith("g_zr"):
+            assert dvl.project_visual_kv_up_kernel(w.T, w.d, w.r, w.L, torch.bfloat16) == 2
         _build_and_projection(w)
     finally:
         dvl.set_fused_kv(False)
+        dvl.set_up_kernel(0)
 
 
 def _build_and_projection(w):
