@@ -290,12 +290,14 @@ def alloc_step(w, Eg, tg):
 def make_step(w, Eg, wg, tg, buf):
     """One pass of the whole path: the all-layer down projection, the memories + norm + K/V of
     every layer, and the attention of every layer. `ev` brackets the three build launches with
-    HIP events, `attn_ev` every attention launch."""
+    HIP events; `attn_span`, a pair of events on torch's current stream (the library's stream
+    here), brackets the attention launches of all layers, which then run back to back as in a
+    timed step."""
     import paper_2609_34972_amd as dvl
 
     Z, Kv, Vv, O = buf["Z"], buf["Kv"], buf["Vv"], buf["O"]
 
-    def step(ev=None, attn_ev=None):
+    def step(ev=None, attn_span=None):
         if ev is not None:
             dvl.time_kernel(dvl.KERNEL_DOWN, *ev["down"])
             dvl.time_kernel(dvl.KERNEL_UP, *ev["up"])
@@ -306,13 +308,13 @@ def make_step(w, Eg, wg, tg, buf):
         if ev is not None:
             for k in (dvl.KERNEL_DOWN, dvl.KERNEL_UP, dvl.KERNEL_KV):
                 dvl.time_kernel(k)
+        if attn_span is not None:
+            attn_span[0].record()
         for l in range(w.L):
-            if attn_ev is not None:
-                dvl.time_kernel(dvl.KERNEL_ATTENTION, *attn_ev[l])
             dvl.text_visual_attention(tg["Q"][l], Kv[l], Vv[l], tg["Kt"][l], tg["Vt"][l], O[l],
                                       q_pos0=w.q_pos0, ws=buf["ws_at"])
-        if attn_ev is not None:
-            dvl.time_kernel(dvl.KERNEL_ATTENTION)
+        if attn_span is not None:
+            attn_span[1].record()
 
     return step
 
@@ -329,8 +331,9 @@ def fused_path(w) -> bool:
 
 def measure_step(w, step, steps, warmup, n_attn_steps=3):
     """Time `steps` whole steps (the three build launches bracketed by HIP events inside the
-    timed region), then time the attention launches in `n_attn_steps` extra steps: events
-    between the 32 short attention launches would add gaps to the timed steps."""
+    timed region), then time the attention launches of every layer in `n_attn_steps` extra steps,
+    back to back between one pair of events (an event pair around each short launch would add
+    its dispatch latency to every launch)."""
     import torch
 
     fused = fused_path(w)
@@ -340,8 +343,8 @@ def measure_step(w, step, steps, warmup, n_attn_steps=3):
     torch.cuda.synchronize()
     hev = HipEvents()
     evs = [{"down": hev.pair(), "up": hev.pair(), "kv": hev.pair()} for _ in range(steps)]
-    attn_evs = [[hev.pair() for _ in range(w.L)] for _ in range(n_attn_steps)]
     mk = lambda: torch.cuda.Event(enable_timing=True)
+    attn_spans = [(mk(), mk()) for _ in range(n_attn_steps)]
     t_begin, t_end = mk(), mk()
     marks = [mk() for _ in range(steps + 1)]
     torch.cuda.synchronize()
@@ -354,12 +357,12 @@ def measure_step(w, step, steps, warmup, n_attn_steps=3):
     torch.cuda.synchronize()
     step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(steps)]
     for s in range(n_attn_steps):
-        step(attn_ev=attn_evs[s])
+        step(attn_span=attn_spans[s])
     torch.cuda.synchronize()
     avg = lambda key: sum(hev.ms(e[key]) for e in evs) / steps
     m = {"ms_step": t_begin.elapsed_time(t_end) / steps, "step_ms": step_ms, "fused": fused,
          "down": avg("down"), "up": 0.0 if fused else avg("up"), "kv": avg("kv"),
-         "attn_launch": sum(hev.ms(a) for e in attn_evs for a in e) / (n_attn_steps * w.L)}
+         "attn_launch": sum(b.elapsed_time(e) for b, e in attn_spans) / (n_attn_steps * w.L)}
     hev.close()
     return m
 
