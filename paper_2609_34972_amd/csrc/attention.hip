@@ -1126,10 +1126,14 @@ AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt,
   const int64_t slots = 256 * (p.nw == 4 ? stream::blocks_per_cu<4>()
                                          : (p.nw == 2 ? stream::blocks_per_cu<2>()
                                                       : stream::blocks_per_cu<1>()));
-  if (p.stream && !p.ksplit && units < slots) {
+  if (p.stream && !p.ksplit && units < 256) {
     // Streaming blocks are LDS-bound (one or two per CU), so they run in rounds of `slots`:
     // take the split count with the fewest tile steps over all rounds,
-    // rounds(units * S) * ceil(tiles / S), preferring fewer splits on ties.
+    // rounds(units * S) * ceil(tiles / S), preferring fewer splits on ties. The model counts a
+    // second block on a CU as doubling its rate, which holds while blocks are short of MFMA work
+    // but not for HBM-bound streams, so keys are split only while some CU would have no block:
+    // LLaVA-NeXT's 256 streams (128 rows per kv-head) ran 84 us per layer unsplit against 88 us
+    // for two half-range blocks per CU and their merge.
     int64_t best = 1, best_cost = tiles;
     const int64_t smax = std::min<int64_t>(64, std::max<int64_t>(1, tiles / 2));
     for (int64_t sp = 2; sp <= smax && sp <= fit; ++sp) {
