@@ -23,18 +23,19 @@ struct AttnArgs {
   int B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0;
   float scale_log2;  // softmax scale times log2(e)
   int splits, keys_per_split;
-  int tiles_per_split;  // bf16 hd-128 prefill: key tiles of 64 per split
+  int tiles_per_split;  // bf16 hd-128 prefill: key tiles per split (32 keys for the key-split
+                        // kernel, 64 for the streaming kernel)
 };
 
 struct AttnPlan {
   bool decode;         // one query per sequence: the bandwidth-bound kernel
   bool stream;         // bf16 hd-128 prefill: direct-to-LDS streaming kernel
   bool ksplit;         // (stream) few rows per kv-head: four waves split the keys of 32 rows
-  int tiles_per_split;  // (stream) 64-key tiles per split
+  int tiles_per_split;  // (stream) key tiles per split: 32 keys each if ksplit, else 64
   int nw;              // waves per block (prefill)
   int row_blocks;      // blocks along the packed (query, head) rows (prefill)
   int splits;          // key splits merged by a log-sum-exp combine
-  int keys_per_split;  // multiple of the 64-key tile
+  int keys_per_split;  // decode and the generic prefill: a multiple of their 64-key tile
   size_t ws_needed;    // bytes of partials for this plan
 };
 
