@@ -26,6 +26,7 @@
 #include <math.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "../../include/deltavision.h"
 
@@ -289,17 +290,17 @@ constexpr int ROWB = HD * 2;              // bytes per K/V row
 constexpr int TILE_BYTES = KT * ROWB;     // one tensor's tile: 16 KiB
 constexpr int STAGE_BYTES = 2 * TILE_BYTES;
 // Stages: up to two tiles keep loading while one is computed. A wave counts at most 63
-// outstanding loads (6-bit vmcnt), i.e. two tiles of a single-wave block. Four-wave blocks
-// keep two stages (64 KiB of LDS) so that two blocks share a CU: one block's softmax (VALU)
-// then overlaps the other's MFMA work.
+// outstanding loads (6-bit vmcnt), i.e. two tiles of a single-wave block. The streaming kernel
+// runs with two waves (65 to 96 rows per kv-head); more rows go to the ping-pong kernel below.
 template <int NW> constexpr int stages() { return NW == 4 ? 2 : 3; }
 // Streaming blocks that fit in one CU's 160 KiB of LDS.
 template <int NW> constexpr int blocks_per_cu() { return (160 * 1024) / (stages<NW>() * 2 * 64 * 256); }
 template <int NW> constexpr int lds_bytes() { return stages<NW>() * STAGE_BYTES; }
 // Cache-policy bits of the tile loads. A K/V tile that only one block reads is loaded
-// non-temporally (LLaVA-NeXT, 128 rows per kv-head: 91.5 -> 81 us per layer); tiles that
-// several row blocks share keep the default policy, so the later readers still find them in
-// the L2 (Qwen2.5-VL video, seven row blocks: non-temporal loads cost about 1.5%).
+// non-temporally (LLaVA-NeXT, 128 rows per kv-head: 91.5 -> 81 us per layer with the four-wave
+// streaming kernel); tiles that several row blocks share keep the default policy, so the later
+// readers still find them in the L2 (Qwen2.5-VL video, seven row blocks: non-temporal loads
+// cost about 1.5%).
 constexpr int CPOL_DEFAULT = 0;
 constexpr int CPOL_NT = 2;
 constexpr int BLOCKS_PER_TILE = KT / 4;   // 1 KiB (4-row) load instructions per tensor
@@ -362,12 +363,16 @@ __device__ __forceinline__ void lds_wait(s16x4 (&v)[N]) {
 // than 2^8: between raises p stays below 256, and since the sum and O use the same stale m the
 // result is unchanged while most tiles skip the rescale of O. The caller adds the tile's p to
 // the row sum l_run (after rounding them for the P V product, see add_probs).
-template <int NI, int NCB>
-__device__ __forceinline__ void online_softmax(float (&sv)[NI], float scale_log2, float& m_run,
+// The scores are the MFMA accumulator tiles themselves, worked on in place (a copy into a plain
+// array cost one move per score: the masking branch made the compiler keep both).
+template <int NB, int NCB>
+__device__ __forceinline__ void online_softmax(f32x16 (&sv)[NB], float scale_log2, float& m_run,
                                                float& l_run, f32x16 (&oacc)[NCB]) {
   float tmax = -INFINITY;
 #pragma unroll
-  for (int i = 0; i < NI; ++i) tmax = fmaxf(tmax, sv[i]);
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sv[b][i]);
   tmax = fmaxf(tmax, shfl_xor(tmax, 32)) * scale_log2;
   const bool grow = tmax > m_run + 8.0f;
   if (__builtin_amdgcn_ballot_w64(grow) != 0) {
@@ -380,7 +385,10 @@ __device__ __forceinline__ void online_softmax(float (&sv)[NI], float scale_log2
   }
   const float neg_m = -m_run;
 #pragma unroll
-  for (int i = 0; i < NI; ++i) sv[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], scale_log2, neg_m));
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      sv[b][i] = __builtin_amdgcn_exp2f(fmaf(sv[b][i], scale_log2, neg_m));
 }
 
 // Adds the eight bf16 probabilities of a P fragment to a row sum: the sum is taken over the
@@ -546,11 +554,6 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
         mfma_k16(sacc[kb], kf, qf[ks]);
       }
     }
-    float scs[32];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) scs[kb * 16 + i] = sacc[kb][i];
     if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask
       // The last key of this tile's kind the lane's row sees, relative to the tile: one compare
       // and select per score.
@@ -559,13 +562,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          scs[kb * 16 + i] = kb * 32 + acc_row(lane, i) > last ? -INFINITY : scs[kb * 16 + i];
+          sacc[kb][i] = kb * 32 + acc_row(lane, i) > last ? -INFINITY : sacc[kb][i];
     }
-    online_softmax<32, HD / 32>(scs, a.scale_log2, m_run, l_run, oacc);
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[kb][i] = scs[kb * 16 + i];
+    online_softmax(sacc, a.scale_log2, m_run, l_run, oacc);
 
     // O^T += V^T P^T. For K step (kb, s2) slot e of lane half g2 is key
     // kb*32 + 16*s2 + (e/4)*8 + 4*g2 + e%4 in both operands; the two transpose loads return
@@ -638,6 +637,284 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void k_attn_stream(AttnAr
       ml[0] = m_run;
       ml[1] = l_tot;
     }
+  }
+}
+
+// ------------------------------------------------------------------ ping-pong streaming prefill
+//
+// Many rows per kv-head (bf16, hd 128): a block of eight waves takes 128 (query, GQA-head) rows.
+// Waves w and w + 4 hold the same 32 rows; the first group of four takes the even key tiles of
+// the block's range, the second the odd ones, and the two partial (max, sum, O) of a row merge
+// through LDS at the end. A group works in alternating phases separated by block barriers: an
+// MFMA phase (P V of its previous tile, then the scores of its next tile) and a softmax phase
+// (the VALU work of that tile's probabilities). The second group runs one phase behind the first,
+// so on every SIMD one wave issues MFMAs while the other works on the VALU: the dependency chain
+// scores -> softmax -> P V of one tile no longer leaves the matrix pipe idle.
+// Each group streams its K tiles and V tiles through rings of two slots; a K tile is read in the
+// MFMA phase that forms its scores and a V tile one MFMA phase later, so every refill has two
+// phases to land. Tiles past the end of a group's share come from an empty buffer range (the
+// loads return zeros without touching memory), so every wave issues the same loads in every
+// phase and one constant wait count holds throughout.
+namespace pp {
+constexpr int HD = 128;
+constexpr int KT = 64;                      // keys per tile
+constexpr int ROWB = HD * 2;
+constexpr int TILE_BYTES = KT * ROWB;       // one tensor's tile: 16 KiB
+constexpr int NRW = 4;                      // waves per group, 32 rows each
+constexpr int NWAVE = 2 * NRW;
+constexpr int GROUP_BYTES = 4 * TILE_BYTES; // two K slots, two V slots
+constexpr int LDS_BYTES = 2 * GROUP_BYTES;  // 128 KiB; the merge reuses it
+constexpr int LD = TILE_BYTES / 1024 / NRW; // 1 KiB loads per wave per tensor tile
+constexpr int MPITCH = HD + 4;              // merge rows padded by 16 B
+static_assert(NRW * 32 * (MPITCH + 2) * 4 <= LDS_BYTES, "merge buffer must fit");
+static_assert(2 * LD <= 63, "vmcnt counts every load in flight");
+}  // namespace pp
+
+template <int CPOL>
+__global__ __launch_bounds__(pp::NWAVE * 64, 1) void k_attn_pp(AttnArgs a, int row_blocks) {
+  using namespace pp;
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int lane = threadIdx.x & 63, wave = wave_index(), g2 = lane >> 5;
+  const int grp = uni(wave / NRW), rw = uni(wave % NRW);
+  const int G = a.Hq / a.Hkv, R = a.Nq * G, n_bg = a.B * a.Hkv;
+
+  const BlockWork wk = block_work(n_bg, row_blocks, a.splits);
+  const int rb = wk.rb, bg = wk.bg, split = wk.split;
+  const int b = uni(bg / a.Hkv), g = bg - b * a.Hkv;
+  const int row0 = rb * 32 * NRW;
+  const int my_row = row0 + rw * 32 + (lane & 31);
+  const bool row_ok = my_row < R;
+  const int my_i = row_ok ? my_row / G : 0;
+  const int my_h = g * G + (row_ok ? my_row - my_i * G : 0);
+  const int i_max = uni((min(row0 + 32 * NRW, R) - 1) / G);
+  const int text_lim = min(a.Nkt, a.q_pos0 + i_max + 1);  // text keys any row of the block needs
+  const int my_text_last = a.q_pos0 + my_i;                // last text key of my row
+  const int tv = uni((a.Nv + KT - 1) / KT), ntiles = uni(tv + (text_lim + KT - 1) / KT);
+  const int t_begin = split * a.tiles_per_split;
+  const int t_end = min(ntiles, t_begin + a.tiles_per_split);
+  const int n = max(0, t_end - t_begin);
+  const int nA = (n + 1) / 2, nB = n / 2;
+  const int nj = grp == 0 ? nA : nB;                     // my group's tiles: t_begin + grp + 2 j
+
+  const bf16* kvb = (const bf16*)a.Kv + (int64_t)bg * a.Nv * HD;
+  const bf16* vvb = (const bf16*)a.Vv + (int64_t)bg * a.Nv * HD;
+  const bf16* ktb = (const bf16*)a.Kt + (int64_t)bg * a.Nkt * HD;
+  const bf16* vtb = (const bf16*)a.Vt + (int64_t)bg * a.Nkt * HD;
+  const int64_t vis_bytes = (int64_t)a.Nv * ROWB, txt_bytes = (int64_t)text_lim * ROWB;
+
+  bf16x8 qf[HD / 16];
+  {
+    const bf16* qrow = (const bf16*)a.Q + (((int64_t)b * a.Nq + my_i) * a.Hq + my_h) * HD;
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks)
+      qf[ks] = row_ok ? __builtin_bit_cast(bf16x8, ld16(qrow + ks * 16 + g2 * 8)) : bf16x8{};
+  }
+
+  unsigned char* gbase = smem + grp * GROUP_BYTES;
+  const int r4 = lane >> 4, pc = lane & 15;
+  // This wave's quarter (4 of the 16 four-row blocks) of K or V of my group's tile j, into ring
+  // slot j % 2. The base and size are selected first (uniform), then the resource is built.
+  auto issue = [&](int j, auto is_v) {
+    constexpr bool V = decltype(is_v)::value;
+    const int t = t_begin + grp + 2 * j;
+    const bool in = j < nj;
+    const bool vis = t < tv;
+    const int key0 = in ? (vis ? t : t - tv) * KT : 0;
+    const bf16* base = vis ? (V ? vvb : kvb) : (V ? vtb : ktb);
+    const int64_t bytes = in ? (vis ? vis_bytes : txt_bytes) : 0;
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(base, bytes);
+    unsigned char* dst = gbase + (V ? 2 * TILE_BYTES : 0) + (j & 1) * TILE_BYTES;
+#pragma unroll
+    for (int i = 0; i < LD; ++i) {
+      const int blk = rw * LD + i;
+      const int row = blk * 4 + r4;
+      const int key = V ? stream::key_v(row) : stream::key_k(row);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + blk * 1024), 16,
+                                               r4 * ROWB + ((pc ^ key) << 4),
+                                               (key0 + blk * 4) * ROWB, 0, CPOL);
+    }
+  };
+  using KTag = std::integral_constant<bool, false>;
+  using VTag = std::integral_constant<bool, true>;
+  // Prologue, oldest first: K of tile 0, then what the steady state issues after MFMA phase k
+  // (K of tile k + 2, V of tile k + 1) for k = -1.
+  issue(0, KTag{});
+  issue(1, KTag{});
+  issue(0, VTag{});
+
+  const int l16 = lane & 15, grp16 = lane >> 4;
+  const int tr_row = l16 >> 2;
+  const int tr_col = 16 * (grp16 & 1) + 4 * (l16 & 3);
+  uint32_t vcol[4];  // as in k_attn_stream
+  {
+    const int vrow = 4 * (grp16 >> 1) + tr_row;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int col = 32 * cb + tr_col;
+      vcol[cb] = vrow * ROWB + (((col >> 3) ^ stream::key_v(vrow)) << 4) + (col & 7) * 2;
+    }
+  }
+
+  f32x16 oacc[HD / 32];
+#pragma unroll
+  for (int cb = 0; cb < HD / 32; ++cb) oacc[cb] = f32x16{};
+  float m_run = NEG_BIG, l_run = 0.f;
+  f32x16 sacc[2];   // scores of the group's newest tile, then its probabilities
+  bf16x8 pb[4];     // probabilities of the previous tile, one fragment per 16-key step
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) sacc[kb] = f32x16{};
+#pragma unroll
+  for (int st = 0; st < 4; ++st) pb[st] = bf16x8{};
+
+  // MFMA phase k: O^T += V^T P^T of tile k - 1, then the scores of tile k.
+  auto mma_phase = [&](int k) {
+    if (k >= 1 && k - 1 < nj) {
+      // V^T fragments in two halves of 32 keys (16 transpose reads each), each waited for just
+      // before its MFMAs.
+      const uint32_t vs = lds_addr(gbase + 2 * TILE_BYTES + ((k - 1) & 1) * TILE_BYTES);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        s16x4 vbuf[2][2 * (HD / 32)];
+        if (h == 0) {
+          read_v_step<ROWB, 0>(vs, vcol, vbuf[0]);
+          read_v_step<ROWB, 16>(vs, vcol, vbuf[1]);
+        } else {
+          read_v_step<ROWB, 32>(vs, vcol, vbuf[0]);
+          read_v_step<ROWB, 48>(vs, vcol, vbuf[1]);
+        }
+        lds_wait(vbuf[0]);
+        lds_wait(vbuf[1]);
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+          for (int cb = 0; cb < HD / 32; ++cb) {
+            const s16x4 vv[2] = {vbuf[s2][2 * cb], vbuf[s2][2 * cb + 1]};
+            mfma_k16(oacc[cb], __builtin_bit_cast(bf16x8, vv), pb[2 * h + s2]);
+          }
+      }
+    }
+    if (k < nj) {
+      const unsigned char* sk = gbase + (k & 1) * TILE_BYTES;
+      // The two 32-key score chains interleaved (K step outer): consecutive MFMAs are independent.
+      sacc[0] = f32x16{};
+      sacc[1] = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < HD / 16; ++ks)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const int row = kb * 32 + (lane & 31);
+          const int chunk = ks * 2 + g2;
+          bf16x8 kf = __builtin_bit_cast(
+              bf16x8, *(const u32x4*)(sk + row * ROWB + ((chunk ^ stream::key_k(row)) << 4)));
+          mfma_k16(sacc[kb], kf, qf[ks]);
+        }
+    }
+  };
+  // Softmax phase k (k >= 0). Every wave of the group finished MFMA phase k (the barrier before
+  // this phase), so the slots of K tile k and V tile k - 1 are free: refill them with K tile
+  // k + 2 and V tile k + 1; then the probabilities of tile k.
+  auto softmax_phase = [&](int k) {
+    issue(k + 2, KTag{});
+    issue(k + 1, VTag{});
+    if (k < nj) {
+      const int t = t_begin + grp + 2 * k;
+      const bool vis = t < tv;
+      const int key0 = (vis ? t : t - tv) * KT;
+      if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask
+        const int last = (vis ? a.Nv - 1 : min(my_text_last, text_lim - 1)) - key0;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            sacc[kb][i] = kb * 32 + acc_row(lane, i) > last ? -INFINITY : sacc[kb][i];
+      }
+      online_softmax(sacc, a.scale_log2, m_run, l_run, oacc);
+      // K step st = (kb, s2) of the P V product takes slots s2 * 8 .. + 7 of key block kb.
+      float lsum[2] = {0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        const int kb = st >> 1, s2 = st & 1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[st][e] = (bf16)sacc[kb][s2 * 8 + e];
+        lsum[s2] = add_probs(pb[st], lsum[s2]);
+      }
+      l_run += lsum[0] + lsum[1];
+    }
+  };
+  // Period q: the first group runs MFMA phase q and then softmax phase q, the second group
+  // softmax phase q - 1 and then MFMA phase q. Before each half every wave has at most its
+  // latest refill (two tiles' loads) in flight, so the tiles of an MFMA phase have landed, and
+  // its LDS reads have returned.
+  // One loop per group, each with two barriers per period, so each wave's program is a plain
+  // sequence of its own phases.
+  const int nq = nA + 1;
+  if (grp == 0) {
+    for (int q = 0; q < nq; ++q) {
+      pipe_sync<waitcnt_imm(2 * LD, 0)>();
+      mma_phase(q);
+      pipe_sync<waitcnt_imm(2 * LD, 0)>();
+      softmax_phase(q);
+    }
+  } else {
+    for (int q = 0; q < nq; ++q) {
+      pipe_sync<waitcnt_imm(2 * LD, 0)>();
+      if (q >= 1) softmax_phase(q - 1);
+      pipe_sync<waitcnt_imm(2 * LD, 0)>();
+      mma_phase(q);
+    }
+  }
+  // The last refills (past the end: zeros) land before the rings are reused for the merge.
+  pipe_sync<waitcnt_imm(0, 0)>();
+
+  const float l_tot = l_run + shfl_xor(l_run, 32);
+  float* red_o = (float*)smem;                 // [NRW][32 rows][MPITCH]: the second group's O^T
+  float* red_ml = red_o + NRW * 32 * MPITCH;   // [NRW][32 rows][2]
+  const int rrow = lane & 31;
+  if (grp == 1) {
+    float* o = red_o + (rw * 32 + rrow) * MPITCH;
+#pragma unroll
+    for (int cb = 0; cb < HD / 32; ++cb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int c = cb * 32 + q4 * 8 + g2 * 4;
+        *(f32x4*)(o + c) = f32x4{oacc[cb][q4 * 4], oacc[cb][q4 * 4 + 1], oacc[cb][q4 * 4 + 2],
+                                 oacc[cb][q4 * 4 + 3]};
+      }
+    if (g2 == 0) {
+      red_ml[(rw * 32 + rrow) * 2] = m_run;
+      red_ml[(rw * 32 + rrow) * 2 + 1] = l_tot;
+    }
+  }
+  __syncthreads();
+  if (grp == 1 || !row_ok) return;  // no barrier follows
+  const float m_o = red_ml[(rw * 32 + rrow) * 2], l_o = red_ml[(rw * 32 + rrow) * 2 + 1];
+  const float mx = fmaxf(m_run, m_o);
+  const float sa = __builtin_amdgcn_exp2f(m_run - mx), sb = __builtin_amdgcn_exp2f(m_o - mx);
+  const float lt = l_tot * sa + l_o * sb;
+  const float* o2 = red_o + (rw * 32 + rrow) * MPITCH;
+  const int64_t orow = ((int64_t)b * a.Nq + my_i) * a.Hq + my_h;
+  const int64_t rows_total = (int64_t)a.B * a.Nq * a.Hq;
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+#pragma unroll
+  for (int cb = 0; cb < HD / 32; ++cb)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int c = cb * 32 + q4 * 8 + g2 * 4;
+      const f32x4 ob = *(const f32x4*)(o2 + c);
+      float y[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) y[u] = oacc[cb][q4 * 4 + u] * sa + ob[u] * sb;
+      if (a.splits == 1)
+        store4<bf16>((bf16*)a.O + orow * HD + c, y[0] * inv, y[1] * inv, y[2] * inv, y[3] * inv);
+      else
+        *(f32x4*)(a.Opart + ((int64_t)split * rows_total + orow) * HD + c) =
+            f32x4{y[0], y[1], y[2], y[3]};
+    }
+  if (a.splits > 1 && g2 == 0) {
+    float* ml = a.MLpart + ((int64_t)split * rows_total + orow) * 2;
+    ml[0] = mx;
+    ml[1] = lt;
   }
 }
 
@@ -762,7 +1039,7 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
     read_v_step<ROWB, 0>(vs, vcol, vr[0]);
     read_v_step<ROWB, 16>(vs, vcol, vr[1]);
 
-    f32x16 sacc = f32x16{};
+    f32x16 sacc[1] = {f32x16{}};
     {
       const int row = lane & 31;
 #pragma unroll
@@ -770,20 +1047,15 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
         const int chunk = ks * 2 + g2;
         bf16x8 kf = __builtin_bit_cast(
             bf16x8, *(const u32x4*)(sk + row * ROWB + ((chunk ^ stream::key_k(row)) << 4)));
-        mfma_k16(sacc, kf, qf[ks]);
+        mfma_k16(sacc[0], kf, qf[ks]);
       }
     }
-    float scs[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) scs[i] = sacc[i];
     if (!vis || key0 + KT > a.Nv) {  // partial visual tile or text tile: mask (as above)
       const int last = (vis ? a.Nv - 1 : min(my_text_last, text_lim - 1)) - key0;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) scs[i] = acc_row(lane, i) > last ? -INFINITY : scs[i];
+      for (int i = 0; i < 16; ++i) sacc[0][i] = acc_row(lane, i) > last ? -INFINITY : sacc[0][i];
     }
-    online_softmax<16, HD / 32>(scs, a.scale_log2, m_run, l_run, oacc);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) sacc[i] = scs[i];
+    online_softmax(sacc, a.scale_log2, m_run, l_run, oacc);
     lds_wait(vr[0]);
     lds_wait(vr[1]);
     float lsum[2] = {0.f, 0.f};
@@ -791,7 +1063,7 @@ __global__ __launch_bounds__(ksplit::NWAVE * 64) void k_attn_ksplit(AttnArgs a, 
     for (int s2 = 0; s2 < 2; ++s2) {
       bf16x8 pf;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[s2 * 8 + e];
+      for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[0][s2 * 8 + e];
       lsum[s2] = add_probs(pf, lsum[s2]);
 #pragma unroll
       for (int cb = 0; cb < HD / 32; ++cb) {
@@ -1104,8 +1376,10 @@ AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt,
       p.row_blocks = (int)cdiv64(R, 32);
       tiles = cdiv64(Nv, 32) + cdiv64(std::min(Nkt, q_pos0 + Nq), 32);
     } else {
-      // Many rows share each K/V tile: blocks of up to 128 rows (four waves), 64-key tiles.
-      p.nw = R <= 96 ? 2 : 4;
+      // Many rows share each K/V tile (64-key tiles): up to 96 rows the two-wave streaming
+      // kernel, above that the ping-pong kernel (blocks of 128 rows).
+      p.pp = R > 96;
+      p.nw = p.pp ? 4 : 2;  // 32-row waves per row block (the ping-pong kernel runs two such groups)
       p.row_blocks = (int)cdiv64(R, 32 * p.nw);
       tiles = cdiv64(Nv, 64) + cdiv64(std::min(Nkt, q_pos0 + Nq), 64);
     }
@@ -1123,17 +1397,15 @@ AttnPlan plan_attention(int B, int Hq, int Hkv, int hd, int Nv, int Nq, int Nkt,
   want = std::min<int64_t>(want, std::max<int64_t>(1, tiles / 2));
   want = std::max<int64_t>(1, std::min<int64_t>(want, 64));
   const int64_t fit = per_split > 0 ? (int64_t)(ws_bytes / (size_t)per_split) : 0;
-  const int64_t slots = 256 * (p.nw == 4 ? stream::blocks_per_cu<4>()
-                                         : (p.nw == 2 ? stream::blocks_per_cu<2>()
-                                                      : stream::blocks_per_cu<1>()));
+  // Both streaming kernels hold one block per CU (LDS), so they run in rounds of 256 blocks.
+  static_assert(stream::blocks_per_cu<2>() == 1, "two-wave streaming blocks: one per CU");
+  const int64_t slots = 256;
   if (p.stream && !p.ksplit && units < 256) {
-    // Streaming blocks are LDS-bound (one or two per CU), so they run in rounds of `slots`:
-    // take the split count with the fewest tile steps over all rounds,
-    // rounds(units * S) * ceil(tiles / S), preferring fewer splits on ties. The model counts a
-    // second block on a CU as doubling its rate, which holds while blocks are short of MFMA work
-    // but not for HBM-bound streams, so keys are split only while some CU would have no block:
-    // LLaVA-NeXT's 256 streams (128 rows per kv-head) ran 84 us per layer unsplit against 88 us
-    // for two half-range blocks per CU and their merge.
+    // Take the split count with the fewest tile steps over all rounds,
+    // rounds(units * S) * ceil(tiles / S), preferring fewer splits on ties. Keys are split only
+    // while some CU would have no block: with four-wave blocks two to a CU, LLaVA-NeXT's 256
+    // streams (128 rows per kv-head) ran 84 us per layer unsplit against 88 us for two
+    // half-range blocks per CU and their merge.
     int64_t best = 1, best_cost = tiles;
     const int64_t smax = std::min<int64_t>(64, std::max<int64_t>(1, tiles / 2));
     for (int64_t sp = 2; sp <= smax && sp <= fit; ++sp) {
@@ -1185,10 +1457,10 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
       static bool once = [] {
         (void)hipFuncSetAttribute((const void*)k_attn_stream<2, CPOL_DEFAULT>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<2>());
-        (void)hipFuncSetAttribute((const void*)k_attn_stream<4, CPOL_DEFAULT>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<4>());
-        (void)hipFuncSetAttribute((const void*)k_attn_stream<4, CPOL_NT>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, stream::lds_bytes<4>());
+        (void)hipFuncSetAttribute((const void*)k_attn_pp<CPOL_DEFAULT>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, pp::LDS_BYTES);
+        (void)hipFuncSetAttribute((const void*)k_attn_pp<CPOL_NT>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, pp::LDS_BYTES);
         return true;
       }();
       (void)once;
@@ -1201,12 +1473,14 @@ static hipError_t attn_launch_t(const AttnArgs& a, const AttnPlan& p, hipStream_
         }();
         (void)once_k;
         k_attn_ksplit<<<grid, dim3(ksplit::NWAVE * 64), ksplit::LDS_BYTES, s>>>(a, p.row_blocks);
-      } else if (p.nw == 2)  // the planner gives the streaming kernel two or four waves
+      } else if (p.pp) {
+        if (p.row_blocks == 1)  // each tile has one reader
+          k_attn_pp<CPOL_NT><<<grid, dim3(pp::NWAVE * 64), pp::LDS_BYTES, s>>>(a, p.row_blocks);
+        else
+          k_attn_pp<CPOL_DEFAULT><<<grid, dim3(pp::NWAVE * 64), pp::LDS_BYTES, s>>>(a, p.row_blocks);
+      } else {
         k_attn_stream<2, CPOL_DEFAULT><<<grid, dim3(128), stream::lds_bytes<2>(), s>>>(a, p.row_blocks);
-      else if (p.row_blocks == 1)  // each tile has one reader
-        k_attn_stream<4, CPOL_NT><<<grid, dim3(256), stream::lds_bytes<4>(), s>>>(a, p.row_blocks);
-      else
-        k_attn_stream<4, CPOL_DEFAULT><<<grid, dim3(256), stream::lds_bytes<4>(), s>>>(a, p.row_blocks);
+      }
     } else {
       return hipErrorInvalidValue;  // the planner only picks this kernel for bf16, hd 128
     }

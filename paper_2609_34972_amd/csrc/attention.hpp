@@ -31,6 +31,7 @@ struct AttnPlan {
   bool decode;         // one query per sequence: the bandwidth-bound kernel
   bool stream;         // bf16 hd-128 prefill: direct-to-LDS streaming kernel
   bool ksplit;         // (stream) few rows per kv-head: four waves split the keys of 32 rows
+  bool pp;             // (stream) over 96 rows per kv-head: the eight-wave ping-pong kernel
   int tiles_per_split;  // (stream) key tiles per split: 32 keys each if ksplit, else 64
   int nw;              // waves per block (prefill)
   int row_blocks;      // blocks along the packed (query, head) rows (prefill)

@@ -72,7 +72,7 @@ int main() {
   expect(dv_text_visual_attention(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 8, 2, 64, 300, 9, 20, 11, -1.f,
                                   DV_BF16, nullptr, 0, nullptr), DV_ERR_SHAPE, "attention scale");
   expect(dv_text_visual_attention_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 64, 8, 128, 4096, 128, 128, 0,
-                                          0.088f, DV_BF16, nullptr), DV_ERR_WORKSPACE, "noalloc beyond scratch");
+                                          0.088f, DV_F32, nullptr), DV_ERR_WORKSPACE, "noalloc beyond scratch");
   expect(dv_text_visual_attention_noalloc(FAKE, nullptr, FAKE, FAKE, FAKE, FAKE, 2, 8, 2, 64, 300, 9, 20, 11,
                                           0.125f, DV_BF16, nullptr), DV_ERR_NULL, "noalloc null");
   (void)dv_text_visual_attention_workspace(64, 32, 32, 128, 576, 1, 513);

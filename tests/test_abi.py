@@ -355,10 +355,10 @@ def noalloc_call(lib, Q=FAKE, Kv=FAKE, Vv=FAKE, Kt=FAKE, Vt=FAKE, O=FAKE, B=2, H
     (dict(Q=None), NULL), (dict(O=None), NULL), (dict(Kv=None), NULL), (dict(O=FAKE + 2), ALIGN),
     (dict(Hq=7), SHAPE), (dict(q0=12), SHAPE), (dict(scale=0.0), SHAPE), (dict(hd=96), UNSUP),
     (dict(dt=3), UNSUP),
-    # 64 GQA streams (8 query heads per key head, 128 text rows): the planner splits the 4096
-    # keys 8 ways, whose partials need more than the static scratch holds, so the call is
-    # refused on the host
-    (dict(B=1, Hq=64, Hkv=8, hd=128, Nv=4096, Nq=128, Nkt=128, q0=0), WS),
+    # fp32 prefill with 64 GQA streams (8 query heads per key head, 128 text rows): the planner
+    # splits the 4096 keys 8 ways, whose partials need more than the static scratch holds, so
+    # the call is refused on the host
+    (dict(B=1, Hq=64, Hkv=8, hd=128, Nv=4096, Nq=128, Nkt=128, q0=0, dt=F32), WS),
 ])
 def test_noalloc_attention_rejects(lib, kw, code):
     assert noalloc_call(lib, **kw) == code

@@ -115,7 +115,7 @@ ATTN = [
     # name, dtype, B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0
     ("llava_mha", "bf16", 2, 8, 8, 128, 577, 64, 64, 0),
     ("qwen_gqa", "bf16", 1, 28, 4, 128, 1000, 128, 128, 0),
-    # 97-128 rows per kv-head: one four-wave streaming block per kv-head, non-temporal tiles
+    # 97-128 rows per kv-head: one ping-pong block (eight waves) per kv-head, non-temporal tiles
     ("next_mha_rows128", "bf16", 2, 8, 8, 128, 700, 128, 128, 0),
     ("ragged_rows100", "bf16", 2, 4, 2, 128, 333, 50, 50, 0),
     ("decode_mha", "bf16", 4, 32, 32, 128, 576, 1, 513, 512),

@@ -76,11 +76,12 @@ def tile_maxima(x, q_pos0, tile):
 
 LAZY = [
     # name, B, Hq, Hkv, hd, Nv, Nq, Nkt: bf16 hd 128 takes the key-group kernel for up to 64
-    # (query, head) rows per kv-head and the streaming kernel above that
+    # (query, head) rows per kv-head, the two-wave streaming kernel for 65-96 and the ping-pong
+    # kernel above that
     ("ksplit_mha", 2, 8, 8, 128, 577, 64, 64),
-    ("stream_gqa", 1, 28, 4, 128, 1000, 128, 128),
+    ("pp_gqa", 1, 28, 4, 128, 1000, 128, 128),
     ("stream_mha_96rows", 2, 6, 2, 128, 700, 32, 32),
-    ("stream_mha_128rows", 2, 8, 8, 128, 700, 128, 128),
+    ("pp_mha_128rows", 2, 8, 8, 128, 700, 128, 128),
 ]
 
 

@@ -57,11 +57,11 @@ def test_noalloc_matches_workspace_entry_point():
 
 
 def test_noalloc_refuses_split_beyond_scratch():
-    # GQA prefill with 64 (kv-head, row block) streams: its preferred split fills 512 blocks of 128
-    # rows, whose fp32 partials need more than the scratch holds
+    # fp32 GQA prefill with 64 (kv-head, row block) streams: its preferred split fills 512 blocks
+    # of 128 rows, whose fp32 partials need more than the scratch holds
     B, Hq, Hkv, hd, Nv, Nq = 1, 64, 8, 128, 4096, 128
     assert dvl.text_visual_attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nq) > dvl.ATTENTION_SCRATCH_BYTES
-    mk = lambda *s: torch.zeros(*s, dtype=torch.bfloat16, device="cuda:0")
+    mk = lambda *s: torch.zeros(*s, dtype=torch.float32, device="cuda:0")
     Q, Kv, Vv, Kt, Vt = mk(B, Nq, Hq, hd), mk(B, Hkv, Nv, hd), mk(B, Hkv, Nv, hd), mk(B, Hkv, Nq, hd), mk(B, Hkv, Nq, hd)
     O = torch.full_like(Q, 7.0)
     with pytest.raises(dvl.DeltaVisionError) as ei:
