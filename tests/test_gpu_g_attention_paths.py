@@ -138,7 +138,8 @@ def test_running_max_rescale_growing_key_norms():
 LONG = [
     # name, dtype, B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0: text keys q_pos0 + Nq .. Nkt - 1 unused
     ("ksplit_chunk", "bf16", 2, 8, 8, 128, 577, 64, 1024, 512),
-    ("stream_chunk", "bf16", 1, 28, 4, 128, 1000, 128, 1024, 512),
+    ("pp_chunk", "bf16", 1, 28, 4, 128, 1000, 128, 1024, 512),
+    ("stream_chunk_96rows", "bf16", 2, 6, 2, 128, 700, 32, 600, 300),
     ("decode_mha", "bf16", 4, 32, 32, 128, 576, 1, 1024, 512),
     ("decode_gqa", "bf16", 2, 28, 4, 128, 300, 1, 1024, 700),
     ("prefill_bf16_hd64", "bf16", 2, 8, 2, 64, 130, 7, 100, 13),
