@@ -178,3 +178,56 @@ def test_text_cache_longer_than_queries(spec, split):
     torch.cuda.synchronize()
     say(f"  err {e:.2e}")
     assert torch.equal(O, O2), "the unused cache slots changed the result"
+
+
+GRAPH = [
+    # name, B, Hq, Hkv, hd, Nv, Nq: both take a key split with the workspace, so the graph holds
+    # the attention kernel and the merge kernel
+    ("ksplit_mha", 1, 4, 4, 128, 577, 64),
+    ("pp_gqa", 1, 28, 4, 128, 1000, 128),
+]
+
+
+@pytest.mark.parametrize("spec", GRAPH, ids=[c[0] for c in GRAPH])
+def test_attention_graph_replays(spec):
+    """A captured HIP graph of an attention call with its key split (the attention kernel, then
+    the merge of the partials in the workspace) replays with eager work in between: every
+    replay, and every eager call after it, gives the bits of the first eager call, which meets
+    the parity bar against the oracle. The workspace starts out filled with a byte pattern."""
+    name, B, Hq, Hkv, hd, Nv, Nq = spec
+    say(f"[graph replays {name}]")
+    n = dvl.text_visual_attention_workspace(B, Hq, Hkv, hd, Nv, Nq, Nq)
+    assert n > 0, "the case must take a key split"
+    g = torch.Generator().manual_seed(29)
+    mk = lambda *s: torch.randn(*s, generator=g).to(torch.bfloat16)
+    x = dict(Q=mk(B, Nq, Hq, hd), Kv=mk(B, Hkv, Nv, hd), Vv=mk(B, Hkv, Nv, hd),
+             Kt=mk(B, Hkv, Nq, hd), Vt=mk(B, Hkv, Nq, hd))
+    xg = {k: cuda(v) for k, v in x.items()}
+    ws = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda:0")
+    args = (xg["Q"], xg["Kv"], xg["Vv"], xg["Kt"], xg["Vt"])
+    O_ref = torch.empty_like(xg["Q"])
+    dvl.text_visual_attention(*args, O_ref, ws=ws)
+    torch.cuda.synchronize()
+    ref = oracle.text_visual_attention(f64(x["Q"]), f64(x["Kv"]), f64(x["Vv"]), f64(x["Kt"]),
+                                       f64(x["Vt"]), 0)
+    assert_close(f64(O_ref), ref, "bf16", f"eager {name}")
+    O = torch.empty_like(O_ref)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        dvl.text_visual_attention(*args, O, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        dvl.text_visual_attention(*args, O, ws=ws)
+    for r in range(4):
+        O.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(O, O_ref), f"replay {r} differs from the eager call"
+        O2 = torch.empty_like(O)
+        dvl.text_visual_attention(*args, O2, ws=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(O2, O_ref), f"eager call after replay {r} differs"
+    say("  4 replays and 4 eager calls equal the first eager call")
