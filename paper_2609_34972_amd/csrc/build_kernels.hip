@@ -223,7 +223,7 @@ __global__ __launch_bounds__(C::NT) void k_kv_proj(const typename C::elem* __res
 // ---------------------------------------------------------------- bf16 pipelined kernels
 
 typedef PipeCfg<128, 128, 2, 2> DownP;  // two blocks per CU
-typedef PipeCfg<96, 128, 2, 2> DownP96;  // two blocks per CU; 2304 x 8192: 1536 tiles, 3 rounds
+typedef PipeCfg<192, 128, 4, 2> DownP192;  // one block per CU; 2304 x 8192: 768 tiles, 3 rounds
 typedef PipeCfg<128, 128, 2, 2> UpP;    // K = r is short; two blocks per CU overlap epilogues
 typedef PipeCfg<256, 256, 4, 2> KvP;    // 9216 tiles of 256 x 256 over 32 LLaVA layers
 // K/V epilogue staging: per wave 64 rows of 128 bf16, rows padded by 16 B.
@@ -316,8 +316,6 @@ struct UpLds {
   static constexpr int BYTES = SS + C::WGN * C::BM * 4;
 };
 
-// Layers per block of the up projection: the block's tile of E is read once for all of them.
-constexpr int kUpLayers = 4;
 
 // One 128 x 128 tile of M_l * gamma_l for kUpLayers consecutive layers through one pipeline
 // (the next layer's first operand tiles load while a layer's epilogue runs). The epilogue works
@@ -333,12 +331,13 @@ __global__ __launch_bounds__(C::NT) void k_up_norm_p(const bf16* __restrict__ E,
                                                        const bf16* __restrict__ gamma,
                                                        bf16* __restrict__ Mg,
                                                        float* __restrict__ ssq, int T, int d,
-                                                       int r, int l0, int nl, int sh, int sw) {
+                                                       int r, int l0, int nl, int lpb, int sh,
+                                                       int sw) {
   static_assert(C::WGN == 2 && C::WN == 64, "epilogue assumes two 64-column wave halves");
   extern __shared__ __align__(16) unsigned char smem[];
   const Tile2 tile = supertile_order(sh, sw);
   const int n0 = tile.nt * C::BN, m0 = tile.mt * C::BM;
-  const int lz0 = blockIdx.z * kUpLayers, nrun = min(nl - lz0, kUpLayers);
+  const int lz0 = blockIdx.z * lpb, nrun = min(nl - lz0, lpb);
   const int ldb = r * 2;
   const int lane = threadIdx.x & 63, wave = wave_index();
   const int wm = wave / C::WGN, wn = wave % C::WGN;
@@ -1056,6 +1055,15 @@ struct TileOrder {
 static TileOrder down_order() { return TileOrder{8, 8}; }
 static TileOrder up_order() { return TileOrder{8, 8}; }
 
+// Layers per block of the tiled up projection. A block reads its tile of E once for all its
+// layers and runs them through one pipeline, which saves E reads and block starts; fewer, longer
+// blocks balance worse over the CUs. Measured (ms, per step): Qwen2.5-VL video 2.27 with 4
+// layers, 2.18 with 8, 2.28-2.40 with 14, 16 or 28; LLaVA-7B 0.31 with 4 or 8, 0.33 with 16.
+static int up_layers_per_block(int64_t tiles_per_layer, int nl) {
+  (void)tiles_per_layer;
+  return std::min(nl, 8);
+}
+
 static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 template <typename T>
@@ -1080,19 +1088,20 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
     static bool once = [] {
       allow_lds(k_down_act_p<KvP, 0>, KvP::LDS_BYTES);
       allow_lds(k_down_act_p<KvP, 1>, KvP::LDS_BYTES);
+      allow_lds(k_down_act_p<DownP192, 0>, DownP192::LDS_BYTES);
+      allow_lds(k_down_act_p<DownP192, 1>, DownP192::LDS_BYTES);
       return true;
     }();
     (void)once;
     const int64_t N = (int64_t)L * r;
     const bool big = cdiv(N, KvP::BN) * cdiv(T_, KvP::BM) >= 4 * 256;
-    // Below that, 128 x 128 or 96 x 128 tiles, whichever needs fewer tile-rounds of the 512
-    // block slots, counting a 96-row tile as 0.8 of a 128-row one (its loads and fragment reads
-    // per MFMA are higher): LLaVA-7B's 2304 x 8192 takes 3 rounds of 96 x 128 tiles against 2.25
-    // (so 3) rounds of 128 x 128 ones.
-    const int64_t slots = 2 * 256;
-    const int64_t r128 = cdiv(cdiv(N, DownP::BN) * cdiv(T_, DownP::BM), slots);
-    const int64_t r96 = cdiv(cdiv(N, DownP96::BN) * cdiv(T_, DownP96::BM), slots);
-    const bool rows96 = !big && 10 * r96 * 96 < 8 * r128 * 128;
+    // Below that, 128 x 128 tiles two blocks per CU, or 192 x 128 tiles of eight waves one block
+    // per CU when they need no more rounds. A 192 x 128 block holds the outputs of two 96 x 128
+    // blocks and loads 28% fewer operand bytes per K step than the two: LLaVA-7B's 2304 x 8192
+    // takes 3 rounds either way, and its down projection went from 0.180 to 0.155 ms.
+    const int64_t r128 = cdiv(cdiv(N, DownP::BN) * cdiv(T_, DownP::BM), 2 * 256);
+    const int64_t r192 = cdiv(cdiv(N, DownP192::BN) * cdiv(T_, DownP192::BM), 256);
+    const bool rows192 = !big && r192 <= r128;
     const TileOrder ord = down_order();
     record(ev.down[0], s);
     if (big) {
@@ -1103,13 +1112,13 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
       else
         k_down_act_p<KvP, 1><<<grid, dim3(KvP::NT), KvP::LDS_BYTES, s>>>((const bf16*)E, (const bf16*)Dw,
                                                                          (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
-    } else if (rows96) {
-      dim3 grid(cdiv(N, DownP96::BN), cdiv(T_, DownP96::BM));
+    } else if (rows192) {
+      dim3 grid(cdiv(N, DownP192::BN), cdiv(T_, DownP192::BM));
       if (act == 0)
-        k_down_act_p<DownP96, 0><<<grid, dim3(DownP96::NT), DownP96::LDS_BYTES, s>>>(
+        k_down_act_p<DownP192, 0><<<grid, dim3(DownP192::NT), DownP192::LDS_BYTES, s>>>(
             (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
       else
-        k_down_act_p<DownP96, 1><<<grid, dim3(DownP96::NT), DownP96::LDS_BYTES, s>>>(
+        k_down_act_p<DownP192, 1><<<grid, dim3(DownP192::NT), DownP192::LDS_BYTES, s>>>(
             (const bf16*)E, (const bf16*)Dw, (bf16*)Z, (int)T_, d, L, r, ord.sh, ord.sw);
     } else {
       dim3 grid(cdiv(N, DownP::BN), cdiv(T_, DownP::BM));
@@ -1234,11 +1243,12 @@ static hipError_t kv_launch_bf16(const void* E, const void* Z, const void* Uw, c
           (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_,
           d, l0, nl);
   } else {
-    dim3 gu(np, cdiv(T_, UpP::BM), cdiv(nl, kUpLayers));
+    const int lpb = up_layers_per_block((int64_t)np * cdiv(T_, UpP::BM), nl);
+    dim3 gu(np, cdiv(T_, UpP::BM), cdiv(nl, lpb));
     const TileOrder uo = up_order();
     k_up_norm_p<UpP><<<gu, dim3(UpP::NT), UpLds<UpP>::BYTES, s>>>(
         (const bf16*)E, (const bf16*)Z, (const bf16*)Uw, (const bf16*)gamma, (bf16*)Mg, ssq, T_,
-        d, r, l0, nl, uo.sh, uo.sw);
+        d, r, l0, nl, lpb, uo.sh, uo.sw);
   }
   if (last) record(ev.up[1], s);
   hipError_t e = hipGetLastError();
