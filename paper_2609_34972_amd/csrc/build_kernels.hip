@@ -1083,8 +1083,13 @@ static hipError_t down_launch(const void* E, const void* Dw, void* Z, int T_, in
 hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, int d, int L,
                            int r, int act, int dtype, hipStream_t s, const LaunchEvents& ev) {
   if (dtype == 1) {
-    // 256 x 256 tiles (one block per CU) once there are at least four rounds of them, so the
-    // last round's tail stays small; 128 x 128 tiles (two blocks per CU) below that.
+    // Three tile shapes; each is priced as rounds of its block slots times the outputs a CU
+    // computes per round, and the cheapest wins, ties going to the larger tile (fewer operand
+    // bytes per MFMA): 256 x 256 (one block per CU), 192 x 128 with eight waves (one block per
+    // CU) and 128 x 128 (two blocks per CU). LLaVA-7B's 2304 x 8192 takes 3 rounds of 192 x 128
+    // (0.180 -> 0.155 ms against the earlier 96 x 128 pairs, bit-identical), LLaVA-NeXT's 23040 x
+    // 8192 30 rounds of 192 x 128 instead of 11.25 of 256 x 256 (1.45-1.49 -> 1.35-1.38 ms), and
+    // Qwen2.5-VL video's 16384 x 14336 14 whole rounds of 256 x 256.
     static bool once = [] {
       allow_lds(k_down_act_p<KvP, 0>, KvP::LDS_BYTES);
       allow_lds(k_down_act_p<KvP, 1>, KvP::LDS_BYTES);
@@ -1094,14 +1099,12 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
     }();
     (void)once;
     const int64_t N = (int64_t)L * r;
-    const bool big = cdiv(N, KvP::BN) * cdiv(T_, KvP::BM) >= 4 * 256;
-    // Below that, 128 x 128 tiles two blocks per CU, or 192 x 128 tiles of eight waves one block
-    // per CU when they need no more rounds. A 192 x 128 block holds the outputs of two 96 x 128
-    // blocks and loads 28% fewer operand bytes per K step than the two: LLaVA-7B's 2304 x 8192
-    // takes 3 rounds either way, and its down projection went from 0.180 to 0.155 ms.
-    const int64_t r128 = cdiv(cdiv(N, DownP::BN) * cdiv(T_, DownP::BM), 2 * 256);
-    const int64_t r192 = cdiv(cdiv(N, DownP192::BN) * cdiv(T_, DownP192::BM), 256);
-    const bool rows192 = !big && r192 <= r128;
+    const int64_t c256 = (int64_t)cdiv(cdiv(N, KvP::BN) * cdiv(T_, KvP::BM), 256) * 256 * 256;
+    const int64_t c192 =
+        (int64_t)cdiv(cdiv(N, DownP192::BN) * cdiv(T_, DownP192::BM), 256) * 192 * 128;
+    const int64_t c128 = (int64_t)cdiv(cdiv(N, DownP::BN) * cdiv(T_, DownP::BM), 512) * 2 * 128 * 128;
+    const bool big = c256 <= c192 && c256 <= c128;
+    const bool rows192 = !big && c192 <= c128;
     const TileOrder ord = down_order();
     record(ev.down[0], s);
     if (big) {
