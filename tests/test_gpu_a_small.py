@@ -111,6 +111,36 @@ def test_project_kv_layer_groups_match_all_layers():
     assert torch.count_nonzero(Kv2[0]) == 0  # layers outside the range are untouched
 
 
+def test_project_kv_eleven_layers_in_runs_of_eight():
+    """The tiled up projection takes up to eight layers per block: 11 layers run as blocks of 8
+    and 3, the sub-range l0 = 2, nl = 9 as 8 and 1, and a one-layer workspace as single layers.
+    All three give the same bytes, and the all-layer call matches the oracle layer by layer."""
+    w = configs.LLAVA7B.with_(name="mid_eleven_layers", d=512, L=11, r=64, Hq=4, Hkv=4, hd=128,
+                              B=2, Nv=150, Nt=8, outlier_channels=(7, 311))
+    say(f"[eleven layers {w.name}: T {w.T}, d {w.d}, r {w.r}]")
+    E, wts = gen_build(w, seed=9)
+    Eg, wg = cuda(E), {k: cuda(v) for k, v in wts.items()}
+    Z, Kv, Vv = run_build(w, Eg, wg, w.act)
+    _, Kv1, Vv1 = run_build(w, Eg, wg, w.act, ws_layers=1)
+    Kv2 = torch.zeros_like(Kv)
+    Vv2 = torch.zeros_like(Vv)
+    ws = torch.empty(dvl.project_visual_kv_workspace(w.T, w.d, 9, Eg.dtype), dtype=torch.uint8,
+                     device="cuda:0")
+    dvl.project_visual_kv(Eg, Z, wg["Uw"], wg["gamma"], wg["Wk"], wg["Wv"], Kv2, Vv2, eps=w.eps,
+                          l0=2, nl=9, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(Kv, Kv1) and torch.equal(Vv, Vv1)
+    assert torch.equal(Kv2[2:], Kv[2:]) and torch.equal(Vv2[2:], Vv[2:])
+    assert torch.count_nonzero(Kv2[:2]) == 0 and torch.count_nonzero(Vv2[:2]) == 0
+    Zr = oracle.down(f64(E), f64(wts["Dw"]), w.act)
+    Kr, Vr = oracle.project_visual_kv(f64(E), Zr, f64(wts["Uw"]), f64(wts["gamma"]), f64(wts["Wk"]),
+                                      f64(wts["Wv"]), w.B, w.Nv, w.Hkv, w.hd, w.eps)
+    for l in range(w.L):
+        assert_close(f64(Z[l]), Zr[l], w.dtype, f"Z layer {l}")
+        assert_close(f64(Kv[l]), Kr[l], w.dtype, f"Kv layer {l}")
+        assert_close(f64(Vv[l]), Vr[l], w.dtype, f"Vv layer {l}")
+
+
 ATTN = [
     # name, dtype, B, Hq, Hkv, hd, Nv, Nq, Nkt, q_pos0
     ("llava_mha", "bf16", 2, 8, 8, 128, 577, 64, 64, 0),
