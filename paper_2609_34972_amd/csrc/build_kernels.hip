@@ -223,7 +223,7 @@ __global__ __launch_bounds__(C::NT) void k_kv_proj(const typename C::elem* __res
 // ---------------------------------------------------------------- bf16 pipelined kernels
 
 typedef PipeCfg<128, 128, 2, 2> DownP;  // two blocks per CU
-typedef PipeCfg<192, 128, 4, 2> DownP192;  // one block per CU; 2304 x 8192: 768 tiles, 3 rounds
+typedef PipeCfg<192, 128, 4, 2> DownP192;  // 80 KiB of LDS, 96 VGPRs: two blocks per CU
 typedef PipeCfg<128, 128, 2, 2> UpP;    // K = r is short; two blocks per CU overlap epilogues
 typedef PipeCfg<256, 256, 4, 2> KvP;    // 9216 tiles of 256 x 256 over 32 LLaVA layers
 // K/V epilogue staging: per wave 64 rows of 128 bf16, rows padded by 16 B.
@@ -1085,10 +1085,11 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
   if (dtype == 1) {
     // Three tile shapes; each is priced as rounds of its block slots times the outputs a CU
     // computes per round, and the cheapest wins, ties going to the larger tile (fewer operand
-    // bytes per MFMA): 256 x 256 (one block per CU), 192 x 128 with eight waves (one block per
-    // CU) and 128 x 128 (two blocks per CU). LLaVA-7B's 2304 x 8192 takes 3 rounds of 192 x 128
-    // (0.180 -> 0.155 ms against the earlier 96 x 128 pairs, bit-identical), LLaVA-NeXT's 23040 x
-    // 8192 30 rounds of 192 x 128 instead of 11.25 of 256 x 256 (1.45-1.49 -> 1.35-1.38 ms), and
+    // bytes per MFMA): 256 x 256 (one block per CU), 192 x 128 with eight waves and 128 x 128
+    // with four (two blocks per CU each; two 192 x 128 blocks take all 160 KiB of LDS, and forcing
+    // one per CU made them 25-35% slower). LLaVA-7B's 2304 x 8192 takes 1.5 rounds of 192 x 128
+    // (0.180 -> 0.149 ms against the earlier 96 x 128 blocks, bit-identical), LLaVA-NeXT's 23040 x
+    // 8192 15 rounds of 192 x 128 instead of 11.25 of 256 x 256 (1.47 -> 1.31-1.41 ms), and
     // Qwen2.5-VL video's 16384 x 14336 14 whole rounds of 256 x 256.
     static bool once = [] {
       allow_lds(k_down_act_p<KvP, 0>, KvP::LDS_BYTES);
@@ -1101,7 +1102,7 @@ hipError_t launch_down_act(const void* E, const void* Dw, void* Z, int64_t T_, i
     const int64_t N = (int64_t)L * r;
     const int64_t c256 = (int64_t)cdiv(cdiv(N, KvP::BN) * cdiv(T_, KvP::BM), 256) * 256 * 256;
     const int64_t c192 =
-        (int64_t)cdiv(cdiv(N, DownP192::BN) * cdiv(T_, DownP192::BM), 256) * 192 * 128;
+        (int64_t)cdiv(cdiv(N, DownP192::BN) * cdiv(T_, DownP192::BM), 512) * 2 * 192 * 128;
     const int64_t c128 = (int64_t)cdiv(cdiv(N, DownP::BN) * cdiv(T_, DownP::BM), 512) * 2 * 128 * 128;
     const bool big = c256 <= c192 && c256 <= c128;
     const bool rows192 = !big && c192 <= c128;

@@ -111,6 +111,23 @@ def test_project_kv_layer_groups_match_all_layers():
     assert torch.count_nonzero(Kv2[0]) == 0  # layers outside the range are untouched
 
 
+def test_down_192_row_tiles_ragged():
+    """T = 2100 tokens against L * r = 4096 columns: 352 tiles of 192 x 128 fill one round of the
+    512 two-per-CU slots, where 128 x 128 tiles would need two and 256 x 256 tiles two of 256,
+    so the launch takes the 192-row tiles; the last row tile holds 180 rows."""
+    w = configs.LLAVA7B.with_(name="mid_down192", d=256, L=16, r=256, Hq=2, Hkv=2, hd=64, B=3,
+                              Nv=700, Nt=8, outlier_channels=(3, 200))
+    say(f"[down 192-row tiles {w.name}: T {w.T} x N {w.L * w.r} x d {w.d}]")
+    E, wts = gen_build(w, seed=13)
+    Eg, Dg = cuda(E), cuda(wts["Dw"])
+    Z = torch.empty(w.L, w.T, w.r, dtype=Eg.dtype, device="cuda:0")
+    dvl.build_visual_memory(Eg, Dg, Z, act=w.act)
+    torch.cuda.synchronize()
+    Zr = oracle.down(f64(E), f64(wts["Dw"]), w.act)
+    for l in range(w.L):
+        assert_close(f64(Z[l]), Zr[l], w.dtype, f"Z layer {l}")
+
+
 def test_project_kv_eleven_layers_in_runs_of_eight():
     """The tiled up projection takes up to eight layers per block: 11 layers run as blocks of 8
     and 3, the sub-range l0 = 2, nl = 9 as 8 and 1, and a one-layer workspace as single layers.
